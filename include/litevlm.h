@@ -1,0 +1,193 @@
+/*
+ * litevlm.h - C ABI of the LiteVLM select + prefill path on MI355X (gfx950).
+ *
+ * Paper: "LiteVLM: A Low-Latency Vision-Language Model Inference Pipeline for
+ * Resource-Constrained Environments" (arXiv 2506.07416).
+ *
+ * Three calls, in pipeline order, all enqueued on one HIP stream:
+ *   litevlm_patch_select      view selection and per-view patch masking
+ *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
+ *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
+ *
+ * Conventions shared by every call
+ *   - Pointers marked "dev" are device pointers owned by the caller; the library
+ *     never allocates, frees or keeps them after the call returns. "host" pointers
+ *     are read during the call only.
+ *   - Device pointers to tensors of Q/K/V/O and the workspace must be 16-byte
+ *     aligned; other device pointers 4-byte aligned (1-byte for uint8 arrays).
+ *     Tensors are dense and row-major in the stated layout (last index fastest).
+ *   - `stream` is a hipStream_t passed as void* (NULL = the null stream). Calls
+ *     only enqueue work and return; results are valid after the stream is
+ *     synchronised. Nothing in the three calls synchronises with the host.
+ *   - Every argument is validated on the host before anything is enqueued. On
+ *     any error status nothing is launched and no output is written.
+ *     LITEVLM_ERR_HIP reports a failed launch; faults inside kernels surface at
+ *     the caller's next synchronisation, as usual in HIP.
+ *   - Results are deterministic: identical inputs give bitwise-identical outputs
+ *     (fixed reduction orders, no floating-point atomics).
+ *   - Calls are reentrant and keep no global mutable state.
+ *
+ * Sequence layout: visual tokens of view v occupy positions
+ * [view_offsets[v], view_offsets[v+1]), views in order, view_offsets[0] = 0,
+ * view_offsets[N] = V_full; text tokens occupy [V_full, S), T = S - V_full.
+ */
+#ifndef LITEVLM_H
+#define LITEVLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LITEVLM_OK = 0,
+  LITEVLM_ERR_NULL_POINTER = 1, /* a required pointer is NULL */
+  LITEVLM_ERR_BAD_SHAPE = 2,    /* a size is out of range or inconsistent */
+  LITEVLM_ERR_BAD_VALUE = 3,    /* a scalar argument is out of range or not finite */
+  LITEVLM_ERR_UNSUPPORTED = 4,  /* valid request this build does not implement */
+  LITEVLM_ERR_MISALIGNED = 5,   /* a pointer violates the alignment rule */
+  LITEVLM_ERR_WORKSPACE = 6,    /* workspace NULL or smaller than required */
+  LITEVLM_ERR_HIP = 7           /* a HIP runtime call or kernel launch failed */
+} litevlm_status_t;
+
+typedef enum {
+  LITEVLM_F32 = 0,      /* IEEE binary32 */
+  LITEVLM_BF16 = 1,     /* bfloat16 */
+  LITEVLM_FP8_E4M3 = 2  /* OCP E4M3FN (bias 7, max 448, no inf), with a per-tensor fp32 scale */
+} litevlm_dtype_t;
+
+/* Limits of this build. */
+#define LITEVLM_MAX_VIEWS 64      /* N */
+#define LITEVLM_MAX_VISUAL 16384  /* V_full (top-k keeps every key of a sample in LDS) */
+#define LITEVLM_MAX_BATCH 256     /* B */
+
+/* Library version as major*10000 + minor*100 + patch. */
+int32_t litevlm_version(void);
+
+/* Static string naming a status code (never NULL). */
+const char* litevlm_status_string(int32_t status);
+
+/*
+ * litevlm_patch_select - view selection and patch masking.
+ *
+ * Paper: Design section, Patch Selection Module paragraph (the final view score
+ * is a weighted sum of a lexical mapping and the module's logits; views scoring
+ * above a threshold are kept, and only their patches proceed); Experiments
+ * section, Training paragraph (only the selected views' patches reach the
+ * vision encoder, hence the LLM).
+ *
+ * Per sample b and view v:
+ *   s_v = w_lexical * lex_v + (1 - w_lexical) * sigmoid(logit_v)   (fp32, no FMA contraction)
+ *   keep_v = (s_v > threshold); if no view passes, the single best view is kept
+ *   (the lowest v among equal best scores).
+ *
+ *   B, N, S            batch, views (1..LITEVLM_MAX_VIEWS), sequence length
+ *   view_offsets_host  host int32 [N+1]: ascending, off[0] = 0, off[N] = V_full <= S
+ *   view_logit         dev fp32 [B, N]: the selection module's per-view logits
+ *   view_lexical       dev fp32 [B, N] lexical scores in [0, 1], or NULL (= 0)
+ *   w_lexical          weight of the lexical term, in [0, 1]
+ *   threshold          keep threshold on the fused score (finite)
+ *   view_keep          dev out uint8 [B, N]: 1 = view kept
+ *   token_keep         dev out uint8 [B, S]: 1 for tokens of kept views and for all text tokens
+ *   n_visual_kept      dev out int32 [B]: V_b, the visual tokens that survive (may be NULL)
+ */
+litevlm_status_t litevlm_patch_select(int32_t B, int32_t N, int32_t S,
+                                      const int32_t* view_offsets_host,
+                                      const float* view_logit, const float* view_lexical,
+                                      float w_lexical, float threshold,
+                                      uint8_t* view_keep, uint8_t* token_keep,
+                                      int32_t* n_visual_kept, void* stream);
+
+/* Bytes of device workspace litevlm_token_score_topk needs for these sizes
+ * (0 when the sizes are invalid). */
+size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full,
+                                          int32_t Hq, int32_t Hkv, int32_t D);
+
+/*
+ * litevlm_token_score_topk - visual-token importance, top-k and compaction.
+ *
+ * Paper: Design section, Token Selection Module paragraph (the first decoder
+ * layer, run standalone, scores visual tokens from self-attention, in the
+ * manner of FastV; pruning happens before the LLM); Results section, Visual
+ * Token Compression paragraph and Table 1 (compression ratio r; token counts).
+ *
+ * Per sample b, with the patch-selected sequence = kept visual tokens (in
+ * order) followed by all T text tokens, V_b = kept visual count:
+ *   score_b(j) = 1/(Hq*T) * sum_h sum_t softmax_j'(q_{t,h} . k_{j',h/G} * scale)[j]
+ *     where text token t sits at position V_b + t of that sequence and its
+ *     causal row spans positions 0..V_b+t; scale = softmax_scale*q_scale*k_scale.
+ *     Visual tokens of dropped views score -INFINITY.
+ *   k_b = min(V_b, floor(keep_ratio*V_b + 1e-6)), in IEEE double.
+ *   Kept visual tokens: the first k_b in (score descending, position ascending)
+ *     order; exactly equal scores keep the lower position.
+ *   Compacted sequence: kept visual positions ascending, then text positions
+ *     V_full..S-1. cu_seqlens[b+1] - cu_seqlens[b] = k_b + T.
+ *
+ *   dtype              LITEVLM_F32, LITEVLM_BF16 or LITEVLM_FP8_E4M3 (Q, K, V, qc, kc, vc)
+ *   B, S, V_full       batch (1..LITEVLM_MAX_BATCH), sequence length, visual tokens (T = S - V_full >= 1)
+ *   Hq, Hkv, D         query heads, KV heads (Hq % Hkv == 0), head dim (64 or 128)
+ *   q                  dev [B, S, Hq, D]
+ *   k                  dev [B, S, Hkv, D]
+ *   v                  dev [B, S, Hkv, D] (may be NULL when vc is NULL)
+ *   softmax_scale      logit scale, normally 1/sqrt(D) (finite, > 0)
+ *   q_scale, k_scale, v_scale   fp8 dequantisation scales (finite, > 0); must be 1 otherwise
+ *   token_keep         dev uint8 [B, S] from litevlm_patch_select, or NULL = all kept;
+ *                      only positions < V_full are read (text is always kept)
+ *   keep_ratio         r in [0, 1]
+ *   scores             dev out fp32 [B, V_full]
+ *   kept_index         dev out int32, capacity B*S: packed compacted positions
+ *                      (positions within the sample), segment b at cu_seqlens[b]
+ *   cu_seqlens         dev out int32 [B+1]
+ *   qc, kc, vc         dev out packed rows of Q, K, V at kept_index, capacity B*S
+ *                      rows of Hq*D / Hkv*D / Hkv*D elements, exact copies of the
+ *                      input bits; each may be NULL to skip that copy
+ *   workspace          dev scratch of litevlm_token_score_topk_workspace() bytes
+ */
+litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                          int32_t Hq, int32_t Hkv, int32_t D,
+                                          const void* q, const void* k, const void* v,
+                                          float softmax_scale, float q_scale, float k_scale,
+                                          float v_scale, const uint8_t* token_keep,
+                                          double keep_ratio, float* scores, int32_t* kept_index,
+                                          int32_t* cu_seqlens, void* qc, void* kc, void* vc,
+                                          void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * litevlm_prefill_attn - causal GQA prefill attention over packed sequences.
+ *
+ * Paper: Introduction and Related Work, Visual Token Compression (prefill
+ * processes the whole sequence, and self-attention's quadratic cost is what
+ * token compression saves); Figure 3b (prefill latency against input tokens,
+ * FP16 and FP8); Experiments section, Deployment paragraph (FP8 PTQ).
+ *
+ * For each sample b (rows cu_seqlens[b]..cu_seqlens[b+1]-1) and query head h:
+ *   O[i,h] = sum_j softmax_j(l_ij) V[j, h/G],  l_ij = q_i . k_j * softmax_scale*q_scale*k_scale,
+ *   keys j <= i when causal (positions within the sample), all keys otherwise;
+ *   the result is multiplied by v_scale. Softmax and accumulation in fp32.
+ *
+ *   in_dtype           LITEVLM_F32, LITEVLM_BF16 or LITEVLM_FP8_E4M3
+ *   out_dtype          LITEVLM_F32 or LITEVLM_BF16 (BF16 is the normal output for BF16/FP8 input)
+ *   B, Hq, Hkv, D      batch, heads (Hq % Hkv == 0), head dim (64 or 128)
+ *   qc                 dev [total, Hq, D]; kc, vc dev [total, Hkv, D]; total = cu_seqlens[B]
+ *   cu_seqlens         dev int32 [B+1], non-decreasing, cu_seqlens[0] = 0
+ *   max_seqlen         host upper bound on every cu_seqlens[b+1]-cu_seqlens[b]; the
+ *                      grid is sized from it and surplus tiles exit at once.
+ *                      Segments longer than max_seqlen are undefined behaviour.
+ *   softmax_scale, q_scale, k_scale, v_scale   finite, > 0; scales must be 1 unless FP8
+ *   causal             1 = causal (the prefill path), 0 = full attention
+ *   o                  dev out [total, Hq, D] in out_dtype
+ */
+litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32_t B,
+                                      int32_t Hq, int32_t Hkv, int32_t D,
+                                      const void* qc, const void* kc, const void* vc,
+                                      const int32_t* cu_seqlens, int32_t max_seqlen,
+                                      float softmax_scale, float q_scale, float k_scale,
+                                      float v_scale, int32_t causal, void* o, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LITEVLM_H */

@@ -198,7 +198,7 @@ def gather_rows(x: np.ndarray, kept_index: np.ndarray, cu_seqlens: np.ndarray) -
 
 def prefill_attention(qc: np.ndarray, kc: np.ndarray, vc: np.ndarray, cu_seqlens: np.ndarray,
                       Hq: int, Hkv: int, scale: float,
-                      rows: Optional[Sequence[int]] = None) -> np.ndarray:
+                      rows: Optional[Sequence[int]] = None, causal: bool = True) -> np.ndarray:
     """LLM prefill self-attention over the compacted sequence (Introduction and
     Related Work: the quadratic self-attention of the prefill stage is what
     token compression saves; Figure 3b). Per sample: O = softmax(Q K^T * scale
@@ -207,6 +207,7 @@ def prefill_attention(qc: np.ndarray, kc: np.ndarray, vc: np.ndarray, cu_seqlens
 
     qc: float64 [total, Hq, D]; kc, vc: float64 [total, Hkv, D] packed by
     cu_seqlens. rows: optional packed row indices to compute (the rest are NaN).
+    causal=False drops the mask (full attention; not part of the prefill path).
     Returns float64 [total, Hq, D].
     """
     total, _, D = qc.shape
@@ -223,6 +224,8 @@ def prefill_attention(qc: np.ndarray, kc: np.ndarray, vc: np.ndarray, cu_seqlens
         if local.size == 0:
             continue
         blocked = np.arange(hi - lo)[None, :] > local[:, None]
+        if not causal:
+            blocked[:] = False
         for h in range(Hq):
             g = h // G
             logits = (qc[lo + local, h, :] @ kc[lo:hi, g, :].T) * scale

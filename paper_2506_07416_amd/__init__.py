@@ -1,0 +1,136 @@
+"""LiteVLM select + prefill hot path on MI355X (gfx950).
+
+Thin Python binding over the C ABI of liblitevlm.so: it checks tensor
+placement and shapes, allocates outputs with PyTorch (device memory and the
+current stream are all PyTorch provides) and passes raw pointers. Every step of
+the path runs in the library's HIP kernels:
+
+    patch_select(...)      view selection and per-view patch masking
+    token_score_topk(...)  visual-token scoring, top-k and gather compaction
+    prefill_attn(...)      causal GQA prefill attention over the packed sequence
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+from typing import Optional, Sequence
+
+import torch
+
+from . import _abi
+from ._abi import LiteVLMError, load  # noqa: F401
+
+__all__ = ["patch_select", "token_score_topk", "prefill_attn", "dtype_code", "workspace_bytes",
+           "LiteVLMError", "load"]
+
+
+def dtype_code(t: torch.dtype) -> int:
+    if t == torch.float32:
+        return _abi.F32
+    if t == torch.bfloat16:
+        return _abi.BF16
+    if t in (torch.float8_e4m3fn, torch.uint8):
+        return _abi.FP8_E4M3
+    raise TypeError(f"unsupported dtype {t}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise ValueError("tensors must live on the GPU")
+    if not t.is_contiguous():
+        raise ValueError("tensors must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(device) -> int:
+    return torch.cuda.current_stream(device).cuda_stream
+
+
+def patch_select(view_logit: torch.Tensor, view_offsets: Sequence[int], S: int,
+                 w_lexical: float = 0.0, threshold: float = 0.5,
+                 view_lexical: Optional[torch.Tensor] = None):
+    """View selection + patch mask. view_logit: fp32 [B, N] on the GPU.
+    Returns (view_keep uint8 [B,N], token_keep uint8 [B,S], n_visual_kept int32 [B])."""
+    lib = load()
+    B, N = view_logit.shape
+    dev = view_logit.device
+    view_keep = torch.empty((B, N), dtype=torch.uint8, device=dev)
+    token_keep = torch.empty((B, S), dtype=torch.uint8, device=dev)
+    n_vis = torch.empty((B,), dtype=torch.int32, device=dev)
+    off = (ctypes.c_int32 * (N + 1))(*[int(x) for x in view_offsets])
+    st = lib.litevlm_patch_select(B, N, S, off, _ptr(view_logit), _ptr(view_lexical),
+                                  float(w_lexical), float(threshold), _ptr(view_keep),
+                                  _ptr(token_keep), _ptr(n_vis), _stream(dev))
+    _abi.check(st, "litevlm_patch_select")
+    return view_keep, token_keep, n_vis
+
+
+def workspace_bytes(B: int, S: int, V_full: int, Hq: int, Hkv: int, D: int) -> int:
+    return int(load().litevlm_token_score_topk_workspace(B, S, V_full, Hq, Hkv, D))
+
+
+def token_score_topk(q: torch.Tensor, k: torch.Tensor, v: Optional[torch.Tensor],
+                     token_keep: Optional[torch.Tensor], keep_ratio: float, V_full: int,
+                     softmax_scale: Optional[float] = None, q_scale: float = 1.0,
+                     k_scale: float = 1.0, v_scale: float = 1.0, gather: bool = True,
+                     workspace: Optional[torch.Tensor] = None, out: Optional[dict] = None) -> dict:
+    """Scores, top-k and compaction. q: [B,S,Hq,D], k/v: [B,S,Hkv,D] (fp32, bf16 or
+    E4M3 bytes). Returns a dict of device tensors: scores [B,V_full] fp32,
+    kept_index [B*S] int32 (packed, valid up to cu_seqlens[B]), cu_seqlens [B+1],
+    and when gather is set qc [B*S,Hq,D], kc/vc [B*S,Hkv,D] (valid rows likewise).
+    ``out`` may supply preallocated tensors under the same keys (plus "workspace")."""
+    lib = load()
+    B, S, Hq, D = q.shape
+    Hkv = k.shape[2]
+    dev = q.device
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    o = dict(out or {})
+    o.setdefault("scores", torch.empty((B, V_full), dtype=torch.float32, device=dev))
+    o.setdefault("kept_index", torch.empty((B * S,), dtype=torch.int32, device=dev))
+    o.setdefault("cu_seqlens", torch.empty((B + 1,), dtype=torch.int32, device=dev))
+    if gather:
+        o.setdefault("qc", torch.empty((B * S, Hq, D), dtype=q.dtype, device=dev))
+        o.setdefault("kc", torch.empty((B * S, Hkv, D), dtype=k.dtype, device=dev))
+        o.setdefault("vc", torch.empty((B * S, Hkv, D), dtype=v.dtype, device=dev))
+    nbytes = workspace_bytes(B, S, V_full, Hq, Hkv, D)
+    ws = workspace if workspace is not None else o.get("workspace")
+    if ws is None:
+        ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    o["workspace"] = ws
+    st = lib.litevlm_token_score_topk(
+        dtype_code(q.dtype), B, S, V_full, Hq, Hkv, D, _ptr(q), _ptr(k), _ptr(v),
+        float(softmax_scale), float(q_scale), float(k_scale), float(v_scale), _ptr(token_keep),
+        float(keep_ratio), _ptr(o["scores"]), _ptr(o["kept_index"]), _ptr(o["cu_seqlens"]),
+        _ptr(o.get("qc")), _ptr(o.get("kc")), _ptr(o.get("vc")), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(dev))
+    _abi.check(st, "litevlm_token_score_topk")
+    return o
+
+
+def prefill_attn(qc: torch.Tensor, kc: torch.Tensor, vc: torch.Tensor, cu_seqlens: torch.Tensor,
+                 max_seqlen: int, B: Optional[int] = None, causal: bool = True,
+                 softmax_scale: Optional[float] = None, q_scale: float = 1.0, k_scale: float = 1.0,
+                 v_scale: float = 1.0, out_dtype: Optional[torch.dtype] = None,
+                 out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Causal GQA attention over packed sequences. qc: [rows,Hq,D], kc/vc: [rows,Hkv,D]
+    with rows >= cu_seqlens[B]. Output [rows,Hq,D] in out_dtype (bf16 by default,
+    fp32 for fp32 input); rows past cu_seqlens[B] are left untouched."""
+    lib = load()
+    rows, Hq, D = qc.shape
+    Hkv = kc.shape[1]
+    if B is None:
+        B = cu_seqlens.numel() - 1
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    if out_dtype is None:
+        out_dtype = torch.float32 if qc.dtype == torch.float32 else torch.bfloat16
+    o = out if out is not None else torch.empty((rows, Hq, D), dtype=out_dtype, device=qc.device)
+    st = lib.litevlm_prefill_attn(
+        dtype_code(qc.dtype), dtype_code(o.dtype), B, Hq, Hkv, D, _ptr(qc), _ptr(kc), _ptr(vc),
+        _ptr(cu_seqlens), int(max_seqlen), float(softmax_scale), float(q_scale), float(k_scale),
+        float(v_scale), 1 if causal else 0, _ptr(o), _stream(qc.device))
+    _abi.check(st, "litevlm_prefill_attn")
+    return o

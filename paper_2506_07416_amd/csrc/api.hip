@@ -1,0 +1,175 @@
+// C ABI of the LiteVLM select + prefill path: host-side validation, workspace
+// sizing and dispatch to the kernel launchers. Every check runs before any
+// HIP call, so an error status means nothing was enqueued or written.
+#include <math.h>
+
+#include "launch.hpp"
+
+using namespace litevlm;
+
+namespace {
+
+constexpr int32_t kVersion = 100;  // 0.1.0
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+bool finite_pos(float x) { return isfinite(x) && x > 0.f; }
+bool valid_dtype(int dt) { return dt == LITEVLM_F32 || dt == LITEVLM_BF16 || dt == LITEVLM_FP8_E4M3; }
+
+litevlm_status_t hip_status(hipError_t e) { return e == hipSuccess ? LITEVLM_OK : LITEVLM_ERR_HIP; }
+
+litevlm_status_t check_score_shape(int32_t B, int32_t S, int32_t V_full, int32_t Hq, int32_t Hkv,
+                                   int32_t D) {
+  if (B < 1 || B > LITEVLM_MAX_BATCH) return LITEVLM_ERR_BAD_SHAPE;
+  if (V_full < 0 || V_full > LITEVLM_MAX_VISUAL || S <= V_full) return LITEVLM_ERR_BAD_SHAPE;
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return LITEVLM_ERR_BAD_SHAPE;
+  if (D != 64 && D != 128) return LITEVLM_ERR_BAD_SHAPE;
+  // keep every index computed in int32 inside range
+  if ((int64_t)B * S * Hq * D > ((int64_t)1 << 40)) return LITEVLM_ERR_BAD_SHAPE;
+  if ((int64_t)B * S > INT32_MAX / 2) return LITEVLM_ERR_BAD_SHAPE;
+  return LITEVLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t litevlm_version(void) { return kVersion; }
+
+const char* litevlm_status_string(int32_t s) {
+  switch (s) {
+    case LITEVLM_OK: return "ok";
+    case LITEVLM_ERR_NULL_POINTER: return "null pointer";
+    case LITEVLM_ERR_BAD_SHAPE: return "bad shape";
+    case LITEVLM_ERR_BAD_VALUE: return "bad value";
+    case LITEVLM_ERR_UNSUPPORTED: return "unsupported";
+    case LITEVLM_ERR_MISALIGNED: return "misaligned pointer";
+    case LITEVLM_ERR_WORKSPACE: return "workspace too small";
+    case LITEVLM_ERR_HIP: return "hip error";
+    default: return "unknown status";
+  }
+}
+
+litevlm_status_t litevlm_patch_select(int32_t B, int32_t N, int32_t S,
+                                      const int32_t* view_offsets_host, const float* view_logit,
+                                      const float* view_lexical, float w_lexical, float threshold,
+                                      uint8_t* view_keep, uint8_t* token_keep,
+                                      int32_t* n_visual_kept, void* stream) {
+  if (!view_offsets_host || !view_logit || !view_keep || !token_keep) return LITEVLM_ERR_NULL_POINTER;
+  if (B < 1 || B > LITEVLM_MAX_BATCH || N < 1 || N > LITEVLM_MAX_VIEWS || S < 1)
+    return LITEVLM_ERR_BAD_SHAPE;
+  ViewOffsets vo;
+  if (view_offsets_host[0] != 0) return LITEVLM_ERR_BAD_SHAPE;
+  for (int v = 0; v <= N; ++v) {
+    vo.off[v] = view_offsets_host[v];
+    if (v > 0 && vo.off[v] < vo.off[v - 1]) return LITEVLM_ERR_BAD_SHAPE;
+  }
+  if (vo.off[N] > S) return LITEVLM_ERR_BAD_SHAPE;
+  if (!(w_lexical >= 0.f && w_lexical <= 1.f) || !isfinite(threshold)) return LITEVLM_ERR_BAD_VALUE;
+  if (!aligned(view_logit, 4) || (view_lexical && !aligned(view_lexical, 4)) ||
+      (n_visual_kept && !aligned(n_visual_kept, 4)))
+    return LITEVLM_ERR_MISALIGNED;
+  return hip_status(launch_patch_select(B, N, S, vo, view_logit, view_lexical, w_lexical, threshold,
+                                        view_keep, token_keep, n_visual_kept,
+                                        static_cast<hipStream_t>(stream)));
+}
+
+size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                          int32_t Hkv, int32_t D) {
+  if (check_score_shape(B, S, V_full, Hq, Hkv, D) != LITEVLM_OK) return 0;
+  return score_workspace_layout(B, S, V_full, Hq, Hkv).total;
+}
+
+litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                          int32_t Hq, int32_t Hkv, int32_t D, const void* q,
+                                          const void* k, const void* v, float softmax_scale,
+                                          float q_scale, float k_scale, float v_scale,
+                                          const uint8_t* token_keep, double keep_ratio,
+                                          float* scores, int32_t* kept_index, int32_t* cu_seqlens,
+                                          void* qc, void* kc, void* vc, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  if (!q || !k || !scores || !kept_index || !cu_seqlens) return LITEVLM_ERR_NULL_POINTER;
+  if (vc && !v) return LITEVLM_ERR_NULL_POINTER;
+  if (!valid_dtype(dtype)) return LITEVLM_ERR_UNSUPPORTED;
+  const litevlm_status_t sh = check_score_shape(B, S, V_full, Hq, Hkv, D);
+  if (sh != LITEVLM_OK) return sh;
+  if (!finite_pos(softmax_scale) || !finite_pos(q_scale) || !finite_pos(k_scale) ||
+      !finite_pos(v_scale))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (dtype != LITEVLM_FP8_E4M3 && (q_scale != 1.f || k_scale != 1.f || v_scale != 1.f))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (!(keep_ratio >= 0.0 && keep_ratio <= 1.0)) return LITEVLM_ERR_BAD_VALUE;
+  const void* big[] = {q, k, v, qc, kc, vc, workspace};
+  for (const void* p : big)
+    if (p && !aligned(p, 16)) return LITEVLM_ERR_MISALIGNED;
+  if (!aligned(scores, 4) || !aligned(kept_index, 4) || !aligned(cu_seqlens, 4))
+    return LITEVLM_ERR_MISALIGNED;
+  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv).total;
+  if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
+
+  ScoreArgs a;
+  a.dtype = dtype;
+  a.B = B;
+  a.S = S;
+  a.V_full = V_full;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.q = q;
+  a.k = k;
+  a.v = v;
+  a.logit_scale_log2 = (float)((double)softmax_scale * q_scale * k_scale * 1.4426950408889634);
+  a.token_keep = token_keep;
+  a.keep_ratio = keep_ratio;
+  a.scores = scores;
+  a.kept_index = kept_index;
+  a.cu_seqlens = cu_seqlens;
+  a.qc = qc;
+  a.kc = kc;
+  a.vc = vc;
+  a.workspace = workspace;
+  return hip_status(launch_token_score_topk(a, static_cast<hipStream_t>(stream)));
+}
+
+litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32_t B, int32_t Hq,
+                                      int32_t Hkv, int32_t D, const void* qc, const void* kc,
+                                      const void* vc, const int32_t* cu_seqlens, int32_t max_seqlen,
+                                      float softmax_scale, float q_scale, float k_scale,
+                                      float v_scale, int32_t causal, void* o, void* stream) {
+  if (!qc || !kc || !vc || !cu_seqlens || !o) return LITEVLM_ERR_NULL_POINTER;
+  if (!valid_dtype(in_dtype) || (out_dtype != LITEVLM_F32 && out_dtype != LITEVLM_BF16))
+    return LITEVLM_ERR_UNSUPPORTED;
+  if (B < 1 || B > LITEVLM_MAX_BATCH || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 ||
+      (D != 64 && D != 128) || max_seqlen < 0)
+    return LITEVLM_ERR_BAD_SHAPE;
+  if ((int64_t)B * max_seqlen > INT32_MAX / 2) return LITEVLM_ERR_BAD_SHAPE;
+  if (causal != 0 && causal != 1) return LITEVLM_ERR_BAD_VALUE;
+  if (!finite_pos(softmax_scale) || !finite_pos(q_scale) || !finite_pos(k_scale) ||
+      !finite_pos(v_scale))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (in_dtype != LITEVLM_FP8_E4M3 && (q_scale != 1.f || k_scale != 1.f || v_scale != 1.f))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (!aligned(qc, 16) || !aligned(kc, 16) || !aligned(vc, 16) || !aligned(o, 16) ||
+      !aligned(cu_seqlens, 4))
+    return LITEVLM_ERR_MISALIGNED;
+  if (in_dtype == LITEVLM_FP8_E4M3) return LITEVLM_ERR_UNSUPPORTED;
+
+  AttnArgs a;
+  a.in_dtype = in_dtype;
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.max_seqlen = max_seqlen;
+  a.causal = causal;
+  a.q = qc;
+  a.k = kc;
+  a.v = vc;
+  a.cu_seqlens = cu_seqlens;
+  a.logit_scale_log2 = (float)((double)softmax_scale * q_scale * k_scale * 1.4426950408889634);
+  a.out_scale = v_scale;
+  a.o = o;
+  return hip_status(launch_prefill_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

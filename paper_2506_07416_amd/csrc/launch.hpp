@@ -1,0 +1,64 @@
+// Host-side launch entry points of the device kernels, called by api.hip after
+// argument validation. Each returns the HIP error of its launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "../../include/litevlm.h"
+
+namespace litevlm {
+
+struct ViewOffsets {
+  int32_t off[LITEVLM_MAX_VIEWS + 1];
+};
+
+hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const float* logit,
+                               const float* lexical, float w, float tau, uint8_t* view_keep,
+                               uint8_t* token_keep, int32_t* n_visual_kept, hipStream_t stream);
+
+// Key tile of the two scoring sweeps.
+constexpr int kScoreKeyTile = 64;
+
+// Workspace of the scoring step, carved from one caller buffer:
+//   rowpart  float2 [B][Hkv][n_kt][R]  per-key-tile (max, sum) of each text row
+//   rowstat  float2 [B][Hkv][R]        merged (max, 1/sum) per text row
+//   colpart  float  [B][Hkv][V_full]   per-KV-group column mass
+// with R = (Hq/Hkv)*T rows per KV group and n_kt = ceil(S / kScoreKeyTile).
+struct ScoreWorkspace {
+  size_t rowpart_off, rowstat_off, colpart_off, total;
+};
+ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv);
+
+struct ScoreArgs {
+  int dtype, B, S, V_full, Hq, Hkv, D;
+  const void* q;
+  const void* k;
+  const void* v;
+  float logit_scale_log2;  // softmax_scale*q_scale*k_scale*log2(e)
+  const uint8_t* token_keep;
+  double keep_ratio;
+  float* scores;
+  int32_t* kept_index;
+  int32_t* cu_seqlens;
+  void* qc;
+  void* kc;
+  void* vc;
+  void* workspace;
+};
+hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream);
+
+struct AttnArgs {
+  int in_dtype, out_dtype, B, Hq, Hkv, D, max_seqlen, causal;
+  const void* q;
+  const void* k;
+  const void* v;
+  const int32_t* cu_seqlens;
+  float logit_scale_log2;  // softmax_scale*q_scale*k_scale*log2(e)
+  float out_scale;         // v_scale
+  void* o;
+};
+hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace litevlm

@@ -1,0 +1,155 @@
+"""C-ABI checks that need no GPU: the library loads, exports every symbol the
+header declares, and rejects bad arguments on the host before any HIP call
+(fake, never-dereferenced device addresses are passed)."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+import paper_2506_07416_amd as lv
+from paper_2506_07416_amd import _abi
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "litevlm.h")
+
+A = 0x7F0000000000          # a 256-byte aligned fake device address (never touched)
+MIS = A + 8                  # 8-byte aligned only
+
+
+def header_symbols():
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"\b(litevlm_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_header_symbol():
+    lib = lv.load()
+    syms = header_symbols()
+    assert set(syms) == set(_abi.SIGNATURES), (syms, sorted(_abi.SIGNATURES))
+    for s in syms:
+        assert hasattr(lib, s), s
+
+
+def test_version_and_status_strings():
+    lib = lv.load()
+    assert lib.litevlm_version() >= 100
+    for code in range(8):
+        assert lib.litevlm_status_string(code)
+    assert lib.litevlm_status_string(99) == b"unknown status"
+
+
+def test_header_constants_match_binding():
+    text = open(HEADER).read()
+    assert int(re.search(r"LITEVLM_MAX_VIEWS (\d+)", text).group(1)) == _abi.MAX_VIEWS
+    assert int(re.search(r"LITEVLM_MAX_VISUAL (\d+)", text).group(1)) == _abi.MAX_VISUAL
+    assert int(re.search(r"LITEVLM_MAX_BATCH (\d+)", text).group(1)) == _abi.MAX_BATCH
+
+
+# ----------------------------------------------------------------------------- patch_select
+
+def ps(B=2, N=3, S=20, off=(0, 4, 8, 12), logit=A, lex=None, w=0.0, tau=0.5, vk=A, tk=A, nv=A):
+    lib = lv.load()
+    offs = None if off is None else (ctypes.c_int32 * len(off))(*off)
+    return lib.litevlm_patch_select(B, N, S, offs, logit, lex, w, tau, vk, tk, nv, None)
+
+
+def test_patch_select_validation():
+    assert ps(logit=None) == _abi.ERR_NULL_POINTER
+    assert ps(off=None) == _abi.ERR_NULL_POINTER
+    assert ps(tk=None) == _abi.ERR_NULL_POINTER
+    assert ps(B=0) == _abi.ERR_BAD_SHAPE
+    assert ps(N=0) == _abi.ERR_BAD_SHAPE
+    assert ps(N=65, off=tuple(range(66))) == _abi.ERR_BAD_SHAPE
+    assert ps(off=(1, 4, 8, 12)) == _abi.ERR_BAD_SHAPE          # must start at 0
+    assert ps(off=(0, 8, 4, 12)) == _abi.ERR_BAD_SHAPE          # must ascend
+    assert ps(off=(0, 4, 8, 21)) == _abi.ERR_BAD_SHAPE          # V_full > S
+    assert ps(w=1.5) == _abi.ERR_BAD_VALUE
+    assert ps(w=float("nan")) == _abi.ERR_BAD_VALUE
+    assert ps(tau=float("inf")) == _abi.ERR_BAD_VALUE
+    assert ps(logit=A + 2) == _abi.ERR_MISALIGNED
+    assert ps(nv=A + 1) == _abi.ERR_MISALIGNED
+
+
+# ----------------------------------------------------------------------------- token_score_topk
+
+def st(dtype=_abi.BF16, B=1, S=100, V=80, Hq=8, Hkv=2, D=128, q=A, k=A, v=A, sm=0.088,
+       qs=1.0, ks=1.0, vs=1.0, keep=A, r=0.5, scores=A, ki=A, cu=A, qc=A, kc=A, vc=A, ws=A,
+       wsb=None):
+    lib = lv.load()
+    if wsb is None:
+        wsb = lib.litevlm_token_score_topk_workspace(B, S, V, Hq, Hkv, D)
+    return lib.litevlm_token_score_topk(dtype, B, S, V, Hq, Hkv, D, q, k, v, sm, qs, ks, vs, keep, r,
+                                        scores, ki, cu, qc, kc, vc, ws, wsb, None)
+
+
+def test_workspace_size():
+    lib = lv.load()
+    n = lib.litevlm_token_score_topk_workspace(1, 6272, 6144, 32, 8, 128)
+    # per-tile row stats + merged row stats + per-group column mass
+    R, n_kt = 4 * 128, math.ceil(6272 / 64)
+    assert n >= 8 * 8 * n_kt * R + 8 * 8 * R + 4 * 8 * 6144
+    assert n % 256 == 0
+    assert lib.litevlm_token_score_topk_workspace(1, 10, 10, 8, 2, 128) == 0    # no text token
+    assert lib.litevlm_token_score_topk_workspace(1, 100, 80, 8, 3, 128) == 0   # Hq % Hkv
+
+
+def test_token_score_topk_validation():
+    assert st(q=None) == _abi.ERR_NULL_POINTER
+    assert st(scores=None) == _abi.ERR_NULL_POINTER
+    assert st(cu=None) == _abi.ERR_NULL_POINTER
+    assert st(v=None) == _abi.ERR_NULL_POINTER                  # vc requested without v
+    assert st(dtype=7) == _abi.ERR_UNSUPPORTED
+    assert st(Hkv=3) == _abi.ERR_BAD_SHAPE
+    assert st(D=96) == _abi.ERR_BAD_SHAPE
+    assert st(S=80) == _abi.ERR_BAD_SHAPE                      # T = 0
+    assert st(V=20000, S=20010) == _abi.ERR_BAD_SHAPE          # beyond the top-k limit
+    assert st(B=0) == _abi.ERR_BAD_SHAPE
+    assert st(B=257) == _abi.ERR_BAD_SHAPE
+    assert st(r=1.5) == _abi.ERR_BAD_VALUE
+    assert st(r=-0.1) == _abi.ERR_BAD_VALUE
+    assert st(r=float("nan")) == _abi.ERR_BAD_VALUE
+    assert st(sm=0.0) == _abi.ERR_BAD_VALUE
+    assert st(qs=2.0) == _abi.ERR_BAD_VALUE                    # scales only for fp8
+    assert st(dtype=_abi.FP8_E4M3, qs=float("inf")) == _abi.ERR_BAD_VALUE
+    assert st(q=MIS) == _abi.ERR_MISALIGNED
+    assert st(qc=MIS) == _abi.ERR_MISALIGNED
+    assert st(ws=MIS) == _abi.ERR_MISALIGNED
+    assert st(ki=A + 2) == _abi.ERR_MISALIGNED
+    assert st(ws=None) == _abi.ERR_WORKSPACE
+    assert st(wsb=16) == _abi.ERR_WORKSPACE
+
+
+# ----------------------------------------------------------------------------- prefill_attn
+
+def pa(ind=_abi.BF16, outd=_abi.BF16, B=2, Hq=8, Hkv=2, D=128, q=A, k=A, v=A, cu=A, ml=100,
+       sm=0.088, qs=1.0, ks=1.0, vs=1.0, causal=1, o=A):
+    lib = lv.load()
+    return lib.litevlm_prefill_attn(ind, outd, B, Hq, Hkv, D, q, k, v, cu, ml, sm, qs, ks, vs,
+                                    causal, o, None)
+
+
+def test_prefill_attn_validation():
+    assert pa(q=None) == _abi.ERR_NULL_POINTER
+    assert pa(cu=None) == _abi.ERR_NULL_POINTER
+    assert pa(o=None) == _abi.ERR_NULL_POINTER
+    assert pa(ind=5) == _abi.ERR_UNSUPPORTED
+    assert pa(outd=_abi.FP8_E4M3) == _abi.ERR_UNSUPPORTED
+    assert pa(Hkv=3) == _abi.ERR_BAD_SHAPE
+    assert pa(D=256) == _abi.ERR_BAD_SHAPE
+    assert pa(B=0) == _abi.ERR_BAD_SHAPE
+    assert pa(ml=-1) == _abi.ERR_BAD_SHAPE
+    assert pa(causal=2) == _abi.ERR_BAD_VALUE
+    assert pa(sm=float("nan")) == _abi.ERR_BAD_VALUE
+    assert pa(vs=0.5) == _abi.ERR_BAD_VALUE
+    assert pa(ind=_abi.FP8_E4M3, qs=-1.0) == _abi.ERR_BAD_VALUE
+    assert pa(o=MIS) == _abi.ERR_MISALIGNED
+    assert pa(k=MIS) == _abi.ERR_MISALIGNED
+    assert pa(cu=A + 1) == _abi.ERR_MISALIGNED
+
+
+def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
+    monkeypatch.setattr(_abi, "_LIB", None)
+    monkeypatch.setattr(_abi, "LIB_PATH", str(tmp_path / "missing.so"))
+    with pytest.raises(ImportError):
+        _abi.load()

@@ -376,6 +376,22 @@ def test_attention_pins():
         assert attention_pins(oracle.prefill_attention, seed) == []
 
 
+def test_noncausal_attention_matches_torch():
+    rng = np.random.default_rng(4)
+    cu = np.array([0, 9, 9, 30], np.int32)
+    qc, kc, vc = rng.standard_normal((30, 6, 8)), rng.standard_normal((30, 2, 8)), rng.standard_normal((30, 2, 8))
+    got = oracle.prefill_attention(qc, kc, vc, cu, 6, 2, 0.4, causal=False)
+    for b in range(3):
+        lo, hi = cu[b], cu[b + 1]
+        if hi == lo:
+            continue
+        qq = torch.from_numpy(qc[lo:hi].transpose(1, 0, 2).copy())
+        kk = torch.from_numpy(kc[lo:hi].transpose(1, 0, 2).copy()).repeat_interleave(3, 0)
+        vv = torch.from_numpy(vc[lo:hi].transpose(1, 0, 2).copy()).repeat_interleave(3, 0)
+        ref = torch.nn.functional.scaled_dot_product_attention(qq, kk, vv, scale=0.4).numpy()
+        assert np.allclose(got[lo:hi], ref.transpose(1, 0, 2), rtol=1e-12, atol=1e-14)
+
+
 def test_attention_rows_subset_matches_full():
     rng = np.random.default_rng(3)
     cu = np.array([0, 7, 20], np.int32)
