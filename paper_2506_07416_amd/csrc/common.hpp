@@ -40,6 +40,36 @@ __device__ __forceinline__ float wave_max_xor(float x, int lanemask) {
   return fmaxf(x, __shfl_xor(x, lanemask, kWave));
 }
 
+// Cross-row exchanges on the gfx950 permlane swaps: the pair returned holds
+// {x[lane], x[lane ^ 16]} (resp. ^ 32) with the lower row first in both lanes,
+// so a sum of the pair is bitwise identical in the two lanes.
+__device__ __forceinline__ float2 pair_xor16(float x) {
+  const auto r = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float2 pair_xor32(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return make_float2(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float max_xor16(float x) { const float2 p = pair_xor16(x); return fmaxf(p.x, p.y); }
+__device__ __forceinline__ float max_xor32(float x) { const float2 p = pair_xor32(x); return fmaxf(p.x, p.y); }
+__device__ __forceinline__ float sum_xor16(float x) { const float2 p = pair_xor16(x); return p.x + p.y; }
+__device__ __forceinline__ float sum_xor32(float x) { const float2 p = pair_xor32(x); return p.x + p.y; }
+
+template <int CTRL>
+__device__ __forceinline__ float dpp(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+// Sum over each row of 16 lanes (xor 1, xor 2, half-mirror, mirror); every
+// lane of the row ends with the same bits.
+__device__ __forceinline__ float row16_sum(float x) {
+  x += dpp<0xB1>(x);   // quad_perm [1,0,3,2]
+  x += dpp<0x4E>(x);   // quad_perm [2,3,0,1]
+  x += dpp<0x141>(x);  // row_half_mirror
+  x += dpp<0x140>(x);  // row_mirror
+  return x;
+}
+
 // OCP E4M3FN byte -> fp32 (exact). Used only where an fp8 operand must be
 // widened for a non-MFMA step.
 __device__ __forceinline__ float e4m3_to_f32(uint32_t b) {

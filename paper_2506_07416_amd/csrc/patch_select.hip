@@ -13,28 +13,35 @@ patch_select_kernel(int N, int S, ViewOffsets vo, const float* __restrict__ logi
                     int32_t* __restrict__ n_visual_kept) {
   const int b = blockIdx.x;
   __shared__ uint8_t keep_s[LITEVLM_MAX_VIEWS];
+  __shared__ float s_s[LITEVLM_MAX_VIEWS];
+  // One thread per view, written as the definition reads: no FMA
+  // contraction and IEEE division, so the decision matches an fp32 evaluation.
+  if (threadIdx.x < N) {
+    const int v = threadIdx.x;
+    const float x = logit[b * N + v];
+    const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-x)));
+    const float lex = lexical ? lexical[b * N + v] : 0.0f;
+    const float s = __fadd_rn(__fmul_rn(w, lex), __fmul_rn(__fsub_rn(1.0f, w), sig));
+    s_s[v] = s;
+    keep_s[v] = (uint8_t)(s > tau);
+  }
+  __syncthreads();
   if (threadIdx.x == 0) {
-    // N <= 64 views: one thread, written as the definition reads. No FMA
-    // contraction, IEEE division, so the decision matches an fp32 evaluation.
-    float best = 0.f;
-    int best_v = 0, any = 0;
+    // if no view passes, keep the best one (lowest index among equal scores)
+    int any = 0, best_v = 0;
     for (int v = 0; v < N; ++v) {
-      const float x = logit[b * N + v];
-      const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-x)));
-      const float lex = lexical ? lexical[b * N + v] : 0.0f;
-      const float s = __fadd_rn(__fmul_rn(w, lex), __fmul_rn(__fsub_rn(1.0f, w), sig));
-      const int k = s > tau;
-      keep_s[v] = (uint8_t)k;
-      any |= k;
-      if (v == 0 || s > best) { best = s; best_v = v; }
+      any |= keep_s[v];
+      if (s_s[v] > s_s[best_v]) best_v = v;
     }
     if (!any) keep_s[best_v] = 1;
+  }
+  __syncthreads();
+  if (threadIdx.x < N) view_keep[b * N + threadIdx.x] = keep_s[threadIdx.x];
+  if (threadIdx.x == 0 && n_visual_kept) {
     int nvis = 0;
-    for (int v = 0; v < N; ++v) {
-      view_keep[b * N + v] = keep_s[v];
+    for (int v = 0; v < N; ++v)
       if (keep_s[v]) nvis += vo.off[v + 1] - vo.off[v];
-    }
-    if (n_visual_kept) n_visual_kept[b] = nvis;
+    n_visual_kept[b] = nvis;
   }
   __syncthreads();
   const int V_full = vo.off[N];
