@@ -42,7 +42,12 @@ def parse():
     ap.add_argument("--sets", type=int, default=4, help="rotating input sets (cold-cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true")
-    ap.add_argument("--keep-ratio", type=float, default=HEADLINE_R)
+    ap.add_argument("--keep-ratio", type=float, default=None,
+                    help="keep ratio of the timed workload (default 0.5 for the 6x1024 workload, "
+                         "the workload's own ratio otherwise)")
+    ap.add_argument("--workload", type=int, default=3, choices=(3, 4, 5),
+                    help="3: 6x1024+128 batch 1 bf16 (the reported line); 4/5: batch-8 ragged bf16/fp8, "
+                         "for profiling")
     return ap.parse_args()
 
 
@@ -114,58 +119,78 @@ def main():
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream(dev)
 
-    def up(x):
-        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+    def up(x, dtype):
+        if dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).to(dev)
+        if dtype == "fp8":
+            return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+        return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
 
-    sets = []
-    for run in range(args.sets):
-        c = synth.config_case(3, run=run)
-        sets.append(dict(case=c, q=up(c.q), k=up(c.k), v=up(c.v),
-                         logit=torch.from_numpy(c.view_logit).to(dev)))
-    case = sets[0]["case"]
+    class Runner:
+        """Preallocated buffers and the three calls of one select + prefill step."""
+
+        def __init__(self, cases):
+            self.sets = [dict(case=c, q=up(c.q, c.dtype), k=up(c.k, c.dtype), v=up(c.v, c.dtype),
+                              logit=torch.from_numpy(c.view_logit).to(dev)) for c in cases]
+            c = cases[0]
+            self.case = c
+            B, S, Hq, Hkv, D, V = c.B, c.S, c.Hq, c.Hkv, c.D, c.V_full
+            t = self.sets[0]["q"].dtype
+            self.outs = dict(scores=torch.empty((B, V), dtype=torch.float32, device=dev),
+                             kept_index=torch.empty((B * S,), dtype=torch.int32, device=dev),
+                             cu_seqlens=torch.empty((B + 1,), dtype=torch.int32, device=dev),
+                             qc=torch.empty((B * S, Hq, D), dtype=t, device=dev),
+                             kc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
+                             vc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
+                             workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D),),
+                                                   dtype=torch.uint8, device=dev))
+            self.o = torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device=dev)
+
+        def step(self, st, r, ev=None):
+            c = self.case
+            if ev is not None:
+                ev[0].record(stream)
+            _, tk, _ = lv.patch_select(st["logit"], c.view_offsets, c.S, c.w_lexical, c.threshold)
+            if ev is not None:
+                ev[1].record(stream)
+            lv.token_score_topk(st["q"], st["k"], st["v"], tk, r, c.V_full, q_scale=c.q_scale,
+                                k_scale=c.k_scale, v_scale=c.v_scale, out=self.outs)
+            if ev is not None:
+                ev[2].record(stream)
+            lv.prefill_attn(self.outs["qc"], self.outs["kc"], self.outs["vc"], self.outs["cu_seqlens"],
+                            c.S, B=c.B, q_scale=c.q_scale, k_scale=c.k_scale, v_scale=c.v_scale,
+                            out=self.o)
+            if ev is not None:
+                ev[3].record(stream)
+
+        def measure(self, r, steps, warmup):
+            for i in range(warmup):
+                self.step(self.sets[i % len(self.sets)], r)
+            torch.cuda.synchronize()
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+            t_start = torch.cuda.Event(enable_timing=True)
+            t_end = torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            t_start.record(stream)
+            for i in range(steps):
+                self.step(self.sets[i % len(self.sets)], r, evs[i])
+            t_end.record(stream)
+            torch.cuda.synchronize()
+            total_ms = t_start.elapsed_time(t_end)
+            per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
+                            for e in evs])
+            cu = self.outs["cu_seqlens"].cpu().numpy()
+            return total_ms / steps, per.mean(axis=0), cu
+
+    if args.workload == 3:
+        main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])
+    else:
+        main_runner = Runner([synth.config_case(args.workload)])
+    if args.keep_ratio is None:
+        args.keep_ratio = HEADLINE_R if args.workload == 3 else main_runner.case.keep_ratio
+    case = main_runner.case
     B, S, Hq, Hkv, D, V, T = case.B, case.S, case.Hq, case.Hkv, case.D, case.V_full, case.T
-    # preallocated outputs shared by all steps
-    outs = dict(scores=torch.empty((B, V), dtype=torch.float32, device=dev),
-                kept_index=torch.empty((B * S,), dtype=torch.int32, device=dev),
-                cu_seqlens=torch.empty((B + 1,), dtype=torch.int32, device=dev),
-                qc=torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device=dev),
-                kc=torch.empty((B * S, Hkv, D), dtype=torch.bfloat16, device=dev),
-                vc=torch.empty((B * S, Hkv, D), dtype=torch.bfloat16, device=dev),
-                workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D),), dtype=torch.uint8,
-                                      device=dev))
-    o_buf = torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device=dev)
-
-    def step(st, r, ev=None):
-        if ev is not None:
-            ev[0].record(stream)
-        _, tk, _ = lv.patch_select(st["logit"], case.view_offsets, S, case.w_lexical, case.threshold)
-        if ev is not None:
-            ev[1].record(stream)
-        lv.token_score_topk(st["q"], st["k"], st["v"], tk, r, V, out=outs)
-        if ev is not None:
-            ev[2].record(stream)
-        lv.prefill_attn(outs["qc"], outs["kc"], outs["vc"], outs["cu_seqlens"], S, B=B, out=o_buf)
-        if ev is not None:
-            ev[3].record(stream)
-
-    def measure(r, steps, warmup):
-        for i in range(warmup):
-            step(sets[i % len(sets)], r)
-        torch.cuda.synchronize()
-        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
-        t_start = torch.cuda.Event(enable_timing=True)
-        t_end = torch.cuda.Event(enable_timing=True)
-        torch.cuda.synchronize()
-        t_start.record(stream)
-        for i in range(steps):
-            step(sets[i % len(sets)], r, evs[i])
-        t_end.record(stream)
-        torch.cuda.synchronize()
-        total_ms = t_start.elapsed_time(t_end)
-        per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
-                        for e in evs])
-        cu = outs["cu_seqlens"].cpu().numpy()
-        return total_ms / steps, per.mean(axis=0), cu
+    measure = main_runner.measure
 
     ms_step, per, cu = measure(args.keep_ratio, args.steps, args.warmup)
     seqlens = np.diff(cu).tolist()
@@ -198,6 +223,27 @@ def main():
                           "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                           "attn_frac_bf16_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
 
+    secondary = []
+    if not args.no_sweep:
+        for cfg, name in ((4, "batch 8 ragged (0-4 of 6 views masked per sample), bf16, keep ratio 0.3"),
+                          (5, "batch 8 ragged, fp8 e4m3 Q/K/V with per-tensor scales, bf16 out, keep ratio 0.25")):
+            rn = Runner([synth.config_case(cfg)])
+            c = rn.case
+            m, p, cu2 = rn.measure(c.keep_ratio, max(10, args.steps // 2), 3)
+            sl = np.diff(cu2).tolist()
+            f = attn_flops(sl, c.Hq, c.D)
+            peak = PEAK_FP8_TFLOPS if c.dtype == "fp8" else PEAK_BF16_TFLOPS
+            secondary.append({"workload": "6 views x 1024 + 128 text, GQA 32/8, D=128, " + name,
+                              "dtype": c.dtype, "compacted_len": sl, "ms_per_step": round(m, 4),
+                              "patch_select_us": round(p[0] * 1e3, 2),
+                              "score_topk_gather_us": round(p[1] * 1e3, 2),
+                              "prefill_attn_us": round(p[2] * 1e3, 2),
+                              "attn_gflop": round(f / 1e9, 2),
+                              "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
+                              "attn_frac_of_dtype_peak": round(f / (p[2] * 1e-3) / 1e12 / peak, 4)})
+            del rn
+            torch.cuda.empty_cache()
+
     line = {
         "metric": METRIC,
         "value": round(ms_step, 4),
@@ -228,6 +274,7 @@ def main():
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "flop_per_launch": fl},
         "sweep": sweep,
+        "secondary": secondary,
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(case, args.keep_ratio)

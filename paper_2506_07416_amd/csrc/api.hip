@@ -151,7 +151,6 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
   if (!aligned(qc, 16) || !aligned(kc, 16) || !aligned(vc, 16) || !aligned(o, 16) ||
       !aligned(cu_seqlens, 4))
     return LITEVLM_ERR_MISALIGNED;
-  if (in_dtype == LITEVLM_FP8_E4M3) return LITEVLM_ERR_UNSUPPORTED;
 
   AttnArgs a;
   a.in_dtype = in_dtype;

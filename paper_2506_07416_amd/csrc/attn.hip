@@ -16,6 +16,8 @@
 // swapped) chosen so that the exponentiated accumulator of S^T is already the
 // B operand of the P.V product, 8 consecutive keys per lane. V is stored
 // transposed in LDS ([d][key]) so its A-operand reads are 16-byte rows.
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
@@ -27,7 +29,7 @@ struct AttnParams {
   const void* v;
   const int32_t* cu;
   void* o;
-  int B, Hq, Hkv, G, n_mtiles;
+  int B, Hq, Hkv, G, n_mtiles, n_work, per_xcd;
   float scale_log2, out_scale;
 };
 
@@ -42,26 +44,74 @@ __device__ __forceinline__ void store_out(void* o, size_t idx, float x) {
   else static_cast<float*>(o)[idx] = x;
 }
 
-template <int D, bool CAUSAL, int OUT>
-__global__ void __launch_bounds__(256)
-attn_fwd_bf16_kernel(AttnParams p) {
+// Key (within the 64-key tile) held by S^T block nb, accumulator row rho.
+// bf16: P.V k-steps of 16 keys, lane half hl holding keys 8*hl..8*hl+7 of a
+// step, so row rho of block nb is key 32*nb + swap23(rho).
+// fp8: one P.V k-step of 64 keys, lane half hl holding keys 32*hl..32*hl+31,
+// so row rho of block nb is key 32*bit2(rho) + 16*nb + 4*(rho>>3) + (rho&3).
+template <bool FP8>
+__device__ __forceinline__ int tile_key(int nb, int rho) {
+  if (FP8) return 32 * ((rho >> 2) & 1) + 16 * nb + 4 * (rho >> 3) + (rho & 3);
+  return 32 * nb + swap23(rho);
+}
+
+// Work item of a flat grid. Items are ordered (KV head, query tile heaviest
+// first, sample, head in group) and dealt to the 8 XCDs in contiguous ranges:
+// an XCD owns whole KV heads across the batch, so workgroups sharing K/V sit
+// behind the same L2 while ragged samples spread evenly over the XCDs, and
+// within an XCD the longest causal tiles start first.
+__device__ __forceinline__ bool decode_work(const AttnParams& p, int& b, int& h, int& mt) {
+  const int L = blockIdx.x;
+  const int w = (L & 7) * p.per_xcd + (L >> 3);
+  if (w >= p.n_work) return false;
+  const int hh = w % p.G;
+  int rest = w / p.G;
+  b = rest % p.B;
+  rest /= p.B;
+  const int mrev = rest % p.n_mtiles;
+  const int g = rest / p.n_mtiles;
+  h = g * p.G + hh;
+  mt = p.n_mtiles - 1 - mrev;
+  return true;
+}
+
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// Flash forward for bf16 (v_mfma_f32_32x32x16_bf16) and OCP E4M3
+// (v_mfma_f32_32x32x64_f8f6f4) inputs. 4 waves x 32 query rows of one head;
+// K and V^T tiles of 64 keys double-buffered in LDS, the next tile fetched
+// into registers while the current one is consumed.
+template <int D, bool CAUSAL, int OUT, bool FP8>
+__global__ void __launch_bounds__(256, 2)
+attn_fwd_kernel(AttnParams p) {
   constexpr int BM = 128, BN = 64;
-  constexpr int KS = D / 16;   // k-steps of S^T (contraction over head dims)
-  constexpr int DB = D / 32;   // 32-row blocks of O^T
-  constexpr int KPAD = D + 8;  // LDS row stride of the K tile [BN][KPAD]
-  constexpr int VPAD = BN + 8; // LDS row stride of the V^T tile [D][VPAD]
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BN * KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D * VPAD];
+  constexpr int EB = FP8 ? 1 : 2;                // bytes per element
+  constexpr int KROW = D * EB + 16;              // padded LDS bytes per K row
+  constexpr int VROW = BN * EB + 16;             // padded LDS bytes per V^T row (one head dim)
+  constexpr int QKS = FP8 ? D / 64 : D / 16;     // k-steps of S^T
+  constexpr int DB = D / 32;                     // 32-row blocks of O^T
+  // Lazy rescale: the running max only moves when it grows by more than TAU
+  // (log2 units). bf16 tolerates p up to 2^8. E4M3 keeps TAU = 0: with the
+  // exact max, p <= 1 and near-max probabilities sit just below a power of
+  // two, where E4M3's relative step is finest. P is quantised as p * 2^PSHIFT.
+  constexpr float TAU = FP8 ? 0.f : 8.f;
+  constexpr int PSHIFT = FP8 ? 8 : 0;
+  constexpr int KPIECES = BN * D * EB / 16;      // 16-byte pieces of a K tile
+  constexpr int KPT = (KPIECES + 255) / 256;     // per thread
+  // V: each thread moves 4 keys x VW bytes of one head-dim range
+  constexpr int VW = FP8 ? 8 : 16;               // bytes per key per thread
+  constexpr int VCH = D * EB / VW;               // head-dim chunks per key
+  constexpr int NPAIR = (BN / 4) * VCH;          // (key quad, chunk) pairs of a V tile
+  constexpr int VPT = (NPAIR + 255) / 256;       // per thread
+  __shared__ __attribute__((aligned(16))) uint8_t Ks[2][BN * KROW];
+  __shared__ __attribute__((aligned(16))) uint8_t Vt[2][D * VROW];
 
-  const uint16_t* __restrict__ q = static_cast<const uint16_t*>(p.q);
-  const uint16_t* __restrict__ k = static_cast<const uint16_t*>(p.k);
-  const uint16_t* __restrict__ v = static_cast<const uint16_t*>(p.v);
-
-  // heaviest query tiles first: the tile index is the slowest grid dimension, reversed
-  const int hb_count = p.Hq * p.B;
-  const int hb = blockIdx.x % hb_count;
-  const int mt = p.n_mtiles - 1 - (int)(blockIdx.x / hb_count);
-  const int h = hb % p.Hq, b = hb / p.Hq;
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const uint8_t* __restrict__ q = static_cast<const uint8_t*>(p.q);
+  const uint8_t* __restrict__ k = static_cast<const uint8_t*>(p.k);
+  const uint8_t* __restrict__ v = static_cast<const uint8_t*>(p.v);
   const int seq0 = p.cu[b];
   const int len = p.cu[b + 1] - seq0;
   const int m0 = mt * BM;
@@ -71,13 +121,27 @@ attn_fwd_bf16_kernel(AttnParams p) {
   const int lq = lane & 31, hl = lane >> 5;
   const int qi = m0 + w * 32 + lq;
   const bool q_ok = qi < len;
+  const size_t kvrow = (size_t)p.Hkv * D * EB;   // bytes between consecutive keys
+  const uint8_t* kbase = k + ((size_t)seq0 * p.Hkv + g) * D * EB;
+  const uint8_t* vbase = v + ((size_t)seq0 * p.Hkv + g) * D * EB;
 
-  bf16x8 qreg[KS];
+  // ---- Q as the B operand of S^T = K Q^T
+  typedef typename std::conditional<FP8, i32x8, bf16x8>::type QOp;
+  QOp qreg[QKS];
   {
-    const uint16_t* qr = q + ((size_t)(seq0 + qi) * p.Hq + h) * D;
+    const uint8_t* qr = q + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * D * EB;
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = q_ok ? *reinterpret_cast<const bf16x8*>(qr + ks * 16 + 8 * hl) : bf16x8{};
+    for (int ks = 0; ks < QKS; ++ks) {
+      if constexpr (FP8) {
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl);
+        const u32x4 hi = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl + 16);
+        const i32x8 t = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                         (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+        qreg[ks] = __builtin_bit_cast(QOp, t);
+      } else {
+        qreg[ks] = __builtin_bit_cast(QOp, *reinterpret_cast<const u32x4*>(qr + (ks * 16 + 8 * hl) * 2));
+      }
+    }
   }
 
   f32x16 o[DB];
@@ -86,107 +150,191 @@ attn_fwd_bf16_kernel(AttnParams p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
   float m_run = -INFINITY, l_run = 0.f;
+  const float c = p.scale_log2;
 
   const int kend = CAUSAL ? min(len, m0 + BM) : len;
+  const int ntiles = (kend + BN - 1) / BN;
   const int wave_q0 = m0 + w * 32;
-  const size_t kvrow = (size_t)p.Hkv * D;
-  const uint16_t* kbase = k + ((size_t)seq0 * p.Hkv + g) * D;
-  const uint16_t* vbase = v + ((size_t)seq0 * p.Hkv + g) * D;
 
-  for (int k0 = 0; k0 < kend; k0 += BN) {
-    __syncthreads();
-    // K tile, row-major
-    for (int c = tid; c < BN * D / 8; c += 256) {
-      const int key = c / (D / 8), d8 = (c % (D / 8)) * 8;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (k0 + key < len) val = *reinterpret_cast<const uint4*>(kbase + (k0 + key) * kvrow + d8);
-      *reinterpret_cast<uint4*>(&Ks[key * KPAD + d8]) = val;
+  // ---- tile loads: K pieces and V (key quad, head-dim chunk) pairs
+  u32x4 kreg[KPT];
+  typedef typename std::conditional<FP8, u32x2, u32x4>::type VLoad;
+  VLoad vreg[VPT][4];
+  auto fetch = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < KPT; ++i) {
+      const int pc = min(tid + 256 * i, KPIECES - 1);
+      const int key = pc / (D * EB / 16), off = (pc % (D * EB / 16)) * 16;
+      const int kk = min(k0 + key, len - 1);  // clamped; rows past len are zeroed on store
+      kreg[i] = *reinterpret_cast<const u32x4*>(kbase + kk * kvrow + off);
     }
-    // V tile, transposed: each thread packs 4 keys x 8 dims into 8 row writes
-    for (int c = tid; c < (BN / 4) * (D / 8); c += 256) {
-      const int kq = c / (D / 8), d8 = (c % (D / 8)) * 8;
-      uint4 r4[4];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int key = 4 * kq + i;
-        r4[i] = (k0 + key < len) ? *reinterpret_cast<const uint4*>(vbase + (k0 + key) * kvrow + d8)
-                                 : make_uint4(0, 0, 0, 0);
-      }
-      const uint16_t* e0 = reinterpret_cast<const uint16_t*>(&r4[0]);
-      const uint16_t* e1 = reinterpret_cast<const uint16_t*>(&r4[1]);
-      const uint16_t* e2 = reinterpret_cast<const uint16_t*>(&r4[2]);
-      const uint16_t* e3 = reinterpret_cast<const uint16_t*>(&r4[3]);
+    for (int i = 0; i < VPT; ++i) {
+      const int pr = min(tid + 256 * i, NPAIR - 1);
+      const int kq = pr / VCH, off = (pr % VCH) * VW;
 #pragma unroll
-      for (int dd = 0; dd < 8; ++dd) {
-        uint2 pk;
-        pk.x = (uint32_t)e0[dd] | ((uint32_t)e1[dd] << 16);
-        pk.y = (uint32_t)e2[dd] | ((uint32_t)e3[dd] << 16);
-        *reinterpret_cast<uint2*>(&Vt[(d8 + dd) * VPAD + 4 * kq]) = pk;
+      for (int u = 0; u < 4; ++u) {
+        const int kk = min(k0 + 4 * kq + u, len - 1);
+        vreg[i][u] = *reinterpret_cast<const VLoad*>(vbase + kk * kvrow + off);
       }
     }
-    __syncthreads();
-    if (CAUSAL && k0 > wave_q0 + 31) continue;  // every key of the tile is after this wave's rows
-
-    f32x16 s[2];
+  };
+  auto store = [&](int buf, int k0) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-#pragma unroll
-      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
-      const uint16_t* krow = &Ks[(nb * 32 + swap23(lq)) * KPAD + 8 * hl];
-#pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8*>(krow + ks * 16), qreg[ks], s[nb], 0, 0, 0);
+    for (int i = 0; i < KPT; ++i) {
+      const int pc = tid + 256 * i;
+      if (pc >= KPIECES) break;
+      const int key = pc / (D * EB / 16), off = (pc % (D * EB / 16)) * 16;
+      const u32x4 z = {0u, 0u, 0u, 0u};
+      *reinterpret_cast<u32x4*>(&Ks[buf][key * KROW + off]) = (k0 + key < len) ? kreg[i] : z;
     }
-
-    const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
-    float mx = -INFINITY;
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int i = 0; i < VPT; ++i) {
+      const int pr = tid + 256 * i;
+      if (pr >= NPAIR) break;
+      const int kq = pr / VCH, off = (pr % VCH) * VW;
+      // transpose: head dim d = off/EB + j gets the 4 keys 4kq..4kq+3
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        float x = s[nb][r] * p.scale_log2;
-        if (need_mask) {
-          const int key = k0 + nb * 32 + swap23(acc_row32(r, hl));
-          if (key >= len || (CAUSAL && key > qi)) x = -INFINITY;
+      for (int j = 0; j < VW / EB; ++j) {
+        uint32_t e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          const bool ok = k0 + 4 * kq + u < len;
+          const uint32_t word = vreg[i][u][(j * EB) / 4];
+          const uint32_t sh = ((j * EB) % 4) * 8;
+          e[u] = ok ? (word >> sh) & (FP8 ? 0xFFu : 0xFFFFu) : 0u;
         }
-        s[nb][r] = x;
-        mx = fmaxf(mx, x);
+        const int d = off / EB + j;
+        if constexpr (FP8) {
+          *reinterpret_cast<uint32_t*>(&Vt[buf][d * VROW + 4 * kq]) =
+              e[0] | (e[1] << 8) | (e[2] << 16) | (e[3] << 24);
+        } else {
+          const u32x2 pk = {e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
+          *reinterpret_cast<u32x2*>(&Vt[buf][d * VROW + 8 * kq]) = pk;
+        }
       }
-    mx = wave_max_xor(mx, 32);
-    const float m_new = fmaxf(m_run, mx);
-    const float m_use = (m_new == -INFINITY) ? 0.f : m_new;
-    const float alpha = exp2f(m_run - m_use);
-    m_run = m_new;
-    float rowsum = 0.f;
-    bf16x8 pb[4];
+    }
+  };
+
+  fetch(0);
+  store(0, 0);
+  __syncthreads();
+
+  for (int t = 0; t < ntiles; ++t) {
+    const int buf = t & 1;
+    const int k0 = t * BN;
+    if (t + 1 < ntiles) fetch(k0 + BN);
+    const bool active = !(CAUSAL && k0 > wave_q0 + 31);  // some key of the tile is visible
+    if (active) {
+      // ---- S^T blocks: 2 x (32 keys x 32 queries)
+      f32x16 s[2];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-      float pv[8];
+      for (int nb = 0; nb < 2; ++nb) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        pv[e] = exp2f(s[kk >> 1][8 * (kk & 1) + e] - m_use);
-        rowsum += pv[e];
+        for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+        const uint8_t* krow = &Ks[buf][tile_key<FP8>(nb, lq) * KROW];
+#pragma unroll
+        for (int ks = 0; ks < QKS; ++ks) {
+          if constexpr (FP8) {
+            const u32x4 lo = *reinterpret_cast<const u32x4*>(krow + ks * 64 + 32 * hl);
+            const u32x4 hi = *reinterpret_cast<const u32x4*>(krow + ks * 64 + 32 * hl + 16);
+            const i32x8 a = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                             (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+            s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
+                a, __builtin_bit_cast(i32x8, qreg[ks]), s[nb], 0, 0, 0, 0, 0, 0);
+          } else {
+            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + (ks * 16 + 8 * hl) * 2));
+            s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, qreg[ks]), s[nb], 0, 0, 0);
+          }
+        }
       }
-      pb[kk] = pack_bf16x8(pv);
+      // ---- mask (edge tiles only) and tile max, in raw logit units
+      const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
+      if (need_mask) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + tile_key<FP8>(nb, acc_row32(r, hl));
+            if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
+          }
+      }
+      float mx = s[0][0];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nb][r]);
+      mx = max_xor32(mx);
+      // ---- lazy rescale
+      const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
+      if (__any(grow)) {
+        const float m_new = grow ? fmaxf(m_run, mx) : m_run;
+        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
+      // ---- P = exp2(s*c - m*c), row sums, MFMA operand
+      float rs = 0.f;
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float e = __builtin_amdgcn_exp2f(fmaf(s[nb][r], c, -mc));
+          s[nb][r] = e;
+          rs += e;
+        }
+      l_run += rs;
+      if constexpr (FP8) {
+        // byte s of the lane's 32-byte operand is key 32*hl + s: block s/16, register s%16
+        constexpr float PS = (float)(1 << PSHIFT);
+        int pw[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int nb = i >> 2, r0 = (i & 3) * 4;
+          int wd = __builtin_amdgcn_cvt_pk_fp8_f32(s[nb][r0] * PS, s[nb][r0 + 1] * PS, 0, false);
+          wd = __builtin_amdgcn_cvt_pk_fp8_f32(s[nb][r0 + 2] * PS, s[nb][r0 + 3] * PS, wd, true);
+          pw[i] = wd;
+        }
+        const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const uint8_t* vrow = &Vt[buf][(db * 32 + lq) * VROW + 32 * hl];
+          const u32x4 lo = *reinterpret_cast<const u32x4*>(vrow);
+          const u32x4 hi = *reinterpret_cast<const u32x4*>(vrow + 16);
+          const i32x8 a = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
+                           (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+          o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, pb, o[db], 0, 0, 0, 0, 0, 0);
+        }
+      } else {
+        bf16x8 pb[4];
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          const int nb = kk >> 1, r0 = 8 * (kk & 1);
+          pb[kk] = bf16x8{(__bf16)s[nb][r0], (__bf16)s[nb][r0 + 1], (__bf16)s[nb][r0 + 2],
+                          (__bf16)s[nb][r0 + 3], (__bf16)s[nb][r0 + 4], (__bf16)s[nb][r0 + 5],
+                          (__bf16)s[nb][r0 + 6], (__bf16)s[nb][r0 + 7]};
+        }
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const uint8_t* vrow = &Vt[buf][(db * 32 + lq) * VROW + 16 * hl];
+#pragma unroll
+          for (int kk = 0; kk < 4; ++kk)
+            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vrow + kk * 32)), pb[kk], o[db], 0, 0, 0);
+        }
+      }
     }
-    l_run = l_run * alpha + rowsum;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-#pragma unroll
-    for (int db = 0; db < DB; ++db) {
-      const uint16_t* vrow = &Vt[(db * 32 + lq) * VPAD + 8 * hl];
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk)
-        o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-            *reinterpret_cast<const bf16x8*>(vrow + kk * 16), pb[kk], o[db], 0, 0, 0);
-    }
+    if (t + 1 < ntiles) store(buf ^ 1, k0 + BN);
+    __syncthreads();
   }
 
-  const float l = l_run + __shfl_xor(l_run, 32, kWave);
-  const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
+  const float l = sum_xor32(l_run);
+  const float inv = (l > 0.f) ? p.out_scale / (l * (float)(1 << PSHIFT)) : 0.f;
   if (q_ok) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
 #pragma unroll
@@ -207,10 +355,8 @@ attn_fwd_f32_kernel(AttnParams p) {
   const float* __restrict__ q = static_cast<const float*>(p.q);
   const float* __restrict__ k = static_cast<const float*>(p.k);
   const float* __restrict__ v = static_cast<const float*>(p.v);
-  const int hb_count = p.Hq * p.B;
-  const int hb = blockIdx.x % hb_count;
-  const int mt = p.n_mtiles - 1 - (int)(blockIdx.x / hb_count);
-  const int h = hb % p.Hq, b = hb / p.Hq;
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
   const int seq0 = p.cu[b];
   const int len = p.cu[b + 1] - seq0;
   const int m0 = mt * 64;
@@ -263,15 +409,17 @@ attn_fwd_f32_kernel(AttnParams p) {
 
 template <int D, bool CAUSAL, int OUT>
 static void launch_typed(const AttnArgs& a, AttnParams& p, hipStream_t stream) {
-  if (a.in_dtype == LITEVLM_BF16) {
-    p.n_mtiles = (a.max_seqlen + 127) / 128;
-    hipLaunchKernelGGL((attn_fwd_bf16_kernel<D, CAUSAL, OUT>), dim3(p.n_mtiles * a.Hq * a.B),
-                       dim3(256), 0, stream, p);
-  } else {
-    p.n_mtiles = (a.max_seqlen + 63) / 64;
-    hipLaunchKernelGGL((attn_fwd_f32_kernel<D, CAUSAL, OUT>), dim3(p.n_mtiles * a.Hq * a.B),
-                       dim3(64), 0, stream, p);
-  }
+  const int bm = a.in_dtype == LITEVLM_F32 ? 64 : 128;
+  p.n_mtiles = (a.max_seqlen + bm - 1) / bm;
+  p.n_work = p.n_mtiles * a.Hq * a.B;
+  p.per_xcd = (p.n_work + 7) / 8;
+  const dim3 grid(8 * p.per_xcd);
+  if (a.in_dtype == LITEVLM_BF16)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OUT, false>), grid, dim3(256), 0, stream, p);
+  else if (a.in_dtype == LITEVLM_FP8_E4M3)
+    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OUT, true>), grid, dim3(256), 0, stream, p);
+  else
+    hipLaunchKernelGGL((attn_fwd_f32_kernel<D, CAUSAL, OUT>), grid, dim3(64), 0, stream, p);
 }
 
 template <int D>

@@ -19,7 +19,6 @@ from parity_util import (bits_of, check_attention, check_selection, log, sample_
 
 pytestmark = pytest.mark.gpu
 
-FP8_ATTENTION = False
 SCORE_RTOL = 1e-5   # diagnostic bound on fp32 score error; selection uses the band rule
 
 
@@ -120,6 +119,10 @@ ATTN_CASES = [
     ([190, 64], 4, 4, 64, "bf16", True, True, "bf16"),
     ([333], 8, 8, 64, "bf16", False, True, "f32"),
     ([700, 130], 32, 8, 128, "bf16", False, False, "bf16"),
+    ([1, 127, 128, 129, 300, 0, 257], 8, 2, 128, "fp8", True, True, "bf16"),
+    ([700], 32, 8, 128, "fp8", True, False, "bf16"),
+    ([190, 64, 5], 4, 4, 64, "fp8", True, True, "f32"),
+    ([333, 64], 8, 4, 128, "fp8", False, True, "f32"),
 ]
 
 
@@ -165,8 +168,6 @@ def test_select_chain_matches_oracle(name):
     g = run_select(case)
     ref = oracle.run_path(case, attention=False)
     identical = check_select(case, g, ref, name)
-    if case.dtype == "fp8" and not FP8_ATTENTION:
-        return
     # attention over the compacted sequence
     cu = g["cu"]
     max_len = int(np.max(np.diff(cu)))
@@ -251,9 +252,20 @@ def test_cfg4_full_size_ragged():
     log(f"  attention on {len(rows)} sampled rows {stats}")
 
 
-def test_cfg5_full_size_selection():
+def test_cfg5_full_size_fp8():
     case = synth.config_case(5)
-    log(f"cfg5 full size selection: B={case.B} fp8")
+    log(f"cfg5 full size: B={case.B} fp8 e4m3, scales {case.q_scale:.3g} {case.k_scale:.3g} {case.v_scale:.3g}")
     g = run_select(case)
     ref = oracle.run_path(case, attention=False)
     check_select(case, g, ref, "cfg5")
+    max_len = int(np.max(np.diff(ref["cu_seqlens"])))
+    qc, kc, vc = (to_device(ref[n], case.dtype) for n in ("qc_bits", "kc_bits", "vc_bits"))
+    o = attention_on(case, qc, kc, vc, ref["cu_seqlens"], max_len)
+    rows = sample_rows(ref["cu_seqlens"], 8, seed=9)
+    q64, k64, v64 = oracle.decode_inputs(case)
+    ref_o = oracle.prefill_attention(oracle.gather_rows(q64, ref["kept_index"], ref["cu_seqlens"]),
+                                     oracle.gather_rows(k64, ref["kept_index"], ref["cu_seqlens"]),
+                                     oracle.gather_rows(v64, ref["kept_index"], ref["cu_seqlens"]),
+                                     ref["cu_seqlens"], case.Hq, case.Hkv, 1 / math.sqrt(case.D), rows=rows)
+    stats = check_attention(to_float64(o)[rows], ref_o[rows], "fp8", "cfg5")
+    log(f"  attention on {len(rows)} sampled rows {stats}")
