@@ -344,6 +344,213 @@ attn_fwd_kernel(AttnParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 path: 4 waves x 32 query rows of one head per workgroup, 64-key tiles
+// double-buffered in LDS. Tiles are copied global -> LDS directly
+// (global_load_lds_dwordx4, no VGPR staging) into XOR-swizzled rows so that
+// the MFMA operand reads are bank-conflict free; V stays row-major and is read
+// transposed with ds_read_b64_tr_b16. Every per-lane offset is computed once,
+// outside the key loop. ~210 VGPRs, so two waves share each SIMD and one
+// wave's softmax overlaps the other's matrix work.
+
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) s16x4 lds_s16x4;
+
+// s_waitcnt immediate: wait until at most n vector-memory operations remain
+// (expcnt and lgkmcnt left unconstrained).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+template <int D, bool CAUSAL, int OUT>
+__global__ void __launch_bounds__(256, 2)
+attn_bf16_kernel(AttnParams p) {
+  constexpr int BN = 64, NW = 4, BM = 128;
+  constexpr int RB = D * 2;                 // bytes per key row
+  constexpr int NP = RB / 16;               // 16-byte pieces per row
+  constexpr int TB = BN * RB;               // bytes per tile
+  constexpr int LI = TB / 1024 / NW;        // direct-copy instructions per wave per tile
+  constexpr int KS = D / 16, DB = D / 32;
+  constexpr float TAU = 8.f;
+  static_assert(LI >= 1 && TB % (1024 * NW) == 0, "tile must split into whole wave copies");
+  // V swizzle: piece ^ 4*(row & 3) keeps the 4 rows x 4 pieces of a transposed
+  // read distinct (D = 64 has only 8 pieces per row: piece ^ 4*(row & 1)).
+  constexpr int VSW = NP >= 16 ? 3 : 1;
+  __shared__ __attribute__((aligned(1024))) uint8_t Kl[2][TB];
+  __shared__ __attribute__((aligned(1024))) uint8_t Vl[2][TB];
+
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int m0 = mt * BM;
+  if (m0 >= len) return;
+  const int g = h / p.G;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lq = lane & 31, hl = lane >> 5;
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const uint32_t kvrow = (uint32_t)p.Hkv * RB;
+  const uint8_t* kbase = static_cast<const uint8_t*>(p.k) + ((size_t)seq0 * p.Hkv + g) * RB;
+  const uint8_t* vbase = static_cast<const uint8_t*>(p.v) + ((size_t)seq0 * p.Hkv + g) * RB;
+  const int qi = m0 + w * 32 + lq;
+  const int wave_q0 = m0 + w * 32;
+
+  // ---- per-lane constants
+  int ld_row[LI];
+  uint32_t ld_kpiece[LI], ld_vpiece[LI];
+#pragma unroll
+  for (int j = 0; j < LI; ++j) {
+    const int slot = (w + NW * j) * 64 + lane;
+    const int r = slot / NP, ph = slot % NP;
+    ld_row[j] = r;
+    ld_kpiece[j] = (uint32_t)(ph ^ (r & (NP - 1))) * 16;
+    ld_vpiece[j] = (uint32_t)(ph ^ (4 * (r & VSW))) * 16;
+  }
+  // K operand of S^T block nb: row 32*nb + swap23(lq), logical piece 2*ks + hl
+  const int rho = swap23(lq);
+  uint32_t koff[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = rho * RB + (((2 * ks + hl) ^ (rho & (NP - 1))) * 16);
+  // (block nb adds 32 rows; row & (NP-1) is unchanged for NP <= 32, so the
+  // swizzle of row 32*nb + rho equals that of rho)
+  // V operand by transposed reads: lane reads row 16*kk + 8*(g16>>1) + 4*hf + (s16>>2),
+  // head-dim block c0 = 8*db + 4*(g16&1) + (s16&3) of 4 elements.
+  const int vrow0 = 8 * (g16 >> 1) + (s16 >> 2);
+  uint32_t voff[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int c0 = 8 * db + 4 * (g16 & 1) + (s16 & 3);
+    voff[db] = vrow0 * RB + (((c0 >> 1) ^ (4 * (vrow0 & VSW))) * 16) + (c0 & 1) * 8;
+  }
+
+  auto copy_tile = [&](int tile, int buf) {
+    const int k0 = tile * BN;
+    const bool full = k0 + BN <= len;
+#pragma unroll
+    for (int j = 0; j < LI; ++j) {
+      const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
+      const uint32_t ro = (uint32_t)key * kvrow;
+      __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
+                                       (__attribute__((address_space(3))) void*)(&Kl[buf][(w + NW * j) * 1024]),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
+                                       (__attribute__((address_space(3))) void*)(&Vl[buf][(w + NW * j) * 1024]),
+                                       16, 0, 0);
+    }
+  };
+
+  bf16x8 qreg[KS];
+  {
+    const uint8_t* qr = static_cast<const uint8_t*>(p.q) + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * RB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qreg[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qr + (ks * 16 + 8 * hl) * 2));
+  }
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = p.scale_log2;
+  const int kend = CAUSAL ? min(len, m0 + BM) : len;
+  const int nt = (kend + BN - 1) / BN;
+
+  copy_tile(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    const int k0 = t * BN;
+    if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);   // buffer last read in step t-1
+    if (!(CAUSAL && k0 > wave_q0 + 31)) {
+      // ---- S^T blocks: 2 x (32 keys x 32 queries)
+      const uint8_t* kl = Kl[buf];
+      f32x16 s[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[ks]));
+          s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[nb], 0, 0, 0);
+        }
+      }
+      // ---- mask (edge tiles only), tile max in raw logit units
+      const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
+      if (need_mask) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * nb + swap23(acc_row32(r, hl));
+            if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
+          }
+      }
+      float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
+      mx = max_xor32(mx);
+      // ---- lazy rescale
+      const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
+      if (__any(grow)) {
+        const float m_new = grow ? fmaxf(m_run, mx) : m_run;
+        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        m_run = m_new;
+      }
+      const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
+      // ---- P = exp2(s*c - m*c) as the B operand of O^T += V^T P^T
+      float rs = 0.f;
+      bf16x8 pb[4];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        float e[8];
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          e[i] = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][8 * (kk & 1) + i], c, -mc));
+          rs += e[i];
+        }
+        pb[kk] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
+                        (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
+      }
+      l_run += rs;
+      const uint8_t* vl = Vl[buf];
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db) {
+          const s16x4 p0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vl + voff[db] + (16 * kk) * RB));
+          const s16x4 p1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vl + voff[db] + (16 * kk + 4) * RB));
+          const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(p0, p1, 0, 1, 2, 3, 4, 5, 6, 7));
+          o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[db], 0, 0, 0);
+        }
+      }
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  const float l = sum_xor32(l_run);
+  const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
+  if (qi < len) {
+    const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) store_out<OUT>(p.o, obase + db * 32 + acc_row32(r, hl), o[db][r] * inv);
+  }
+}
+
 // fp32 path: one lane per query row, K/V tiles of 64 keys staged in LDS,
 // plain FMAs. Meant for small fp32 problems.
 template <int D, bool CAUSAL, int OUT>
@@ -415,7 +622,7 @@ static void launch_typed(const AttnArgs& a, AttnParams& p, hipStream_t stream) {
   p.per_xcd = (p.n_work + 7) / 8;
   const dim3 grid(8 * p.per_xcd);
   if (a.in_dtype == LITEVLM_BF16)
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OUT, false>), grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL((attn_bf16_kernel<D, CAUSAL, OUT>), grid, dim3(256), 0, stream, p);
   else if (a.in_dtype == LITEVLM_FP8_E4M3)
     hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OUT, true>), grid, dim3(256), 0, stream, p);
   else
