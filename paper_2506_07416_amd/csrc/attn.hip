@@ -1,21 +1,20 @@
 // Causal GQA prefill attention over packed variable-length sequences: the
 // quadratic part of the LLM prefill that token compression shrinks
-// (Introduction; Related Work, Visual Token Compression; Figure 3b).
+// (Introduction; Related Work, Visual Token Compression; Figure 3b; FP8 from
+// the Experiments section, Deployment paragraph).
 //
-// bf16 path: flash-style forward on v_mfma_f32_32x32x16_bf16 with fp32
-// accumulation and an online softmax in the exp2 domain. A workgroup owns 128
-// query rows of one query head (4 waves x 32 rows) and streams the keys of its
-// KV head in tiles of 64 through LDS.
+// Flash-style forward with fp32 accumulation and an online softmax in the
+// exp2 domain. A workgroup owns 128 query rows of one query head (4 waves x 32
+// rows) and streams the keys of its KV head in 64-key tiles through LDS.
 //
 // Both products are formed transposed so that a lane owns one query row
 // throughout: S^T = K Q^T puts query (lane % 32) in the accumulator columns,
 // and O^T = V^T P^T keeps the same ownership for the output, so the running
 // max / sum / rescale of a row never leave the two lanes (lane, lane ^ 32)
-// that hold it. Q stays in registers as the B operand. K rows are read from
-// LDS as the A operand in a permuted order (bits 2 and 3 of the row index
-// swapped) chosen so that the exponentiated accumulator of S^T is already the
-// B operand of the P.V product, 8 consecutive keys per lane. V is stored
-// transposed in LDS ([d][key]) so its A-operand reads are 16-byte rows.
+// that hold it. Q stays in registers as the B operand. K rows are read as the
+// A operand in a permuted order chosen so that the exponentiated accumulator
+// of S^T is already the B operand of the P.V product; V stays row-major in LDS
+// and the LDS transpose reads (ds_read_b64_tr_b16 / _b8) build its A operand.
 #include <type_traits>
 
 #include "common.hpp"
@@ -77,272 +76,6 @@ __device__ __forceinline__ bool decode_work(const AttnParams& p, int& b, int& h,
 
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
-
-// Flash forward for bf16 (v_mfma_f32_32x32x16_bf16) and OCP E4M3
-// (v_mfma_f32_32x32x64_f8f6f4) inputs. 4 waves x 32 query rows of one head;
-// K and V^T tiles of 64 keys double-buffered in LDS, the next tile fetched
-// into registers while the current one is consumed.
-template <int D, bool CAUSAL, int OUT, bool FP8>
-__global__ void __launch_bounds__(256, 2)
-attn_fwd_kernel(AttnParams p) {
-  constexpr int BM = 128, BN = 64;
-  constexpr int EB = FP8 ? 1 : 2;                // bytes per element
-  constexpr int KROW = D * EB + 16;              // padded LDS bytes per K row
-  constexpr int VROW = BN * EB + 16;             // padded LDS bytes per V^T row (one head dim)
-  constexpr int QKS = FP8 ? D / 64 : D / 16;     // k-steps of S^T
-  constexpr int DB = D / 32;                     // 32-row blocks of O^T
-  // Lazy rescale: the running max only moves when it grows by more than TAU
-  // (log2 units). bf16 tolerates p up to 2^8. E4M3 keeps TAU = 0: with the
-  // exact max, p <= 1 and near-max probabilities sit just below a power of
-  // two, where E4M3's relative step is finest. P is quantised as p * 2^PSHIFT.
-  constexpr float TAU = FP8 ? 0.f : 8.f;
-  constexpr int PSHIFT = FP8 ? 8 : 0;
-  constexpr int KPIECES = BN * D * EB / 16;      // 16-byte pieces of a K tile
-  constexpr int KPT = (KPIECES + 255) / 256;     // per thread
-  // V: each thread moves 4 keys x VW bytes of one head-dim range
-  constexpr int VW = FP8 ? 8 : 16;               // bytes per key per thread
-  constexpr int VCH = D * EB / VW;               // head-dim chunks per key
-  constexpr int NPAIR = (BN / 4) * VCH;          // (key quad, chunk) pairs of a V tile
-  constexpr int VPT = (NPAIR + 255) / 256;       // per thread
-  __shared__ __attribute__((aligned(16))) uint8_t Ks[2][BN * KROW];
-  __shared__ __attribute__((aligned(16))) uint8_t Vt[2][D * VROW];
-
-  int b, h, mt;
-  if (!decode_work(p, b, h, mt)) return;
-  const uint8_t* __restrict__ q = static_cast<const uint8_t*>(p.q);
-  const uint8_t* __restrict__ k = static_cast<const uint8_t*>(p.k);
-  const uint8_t* __restrict__ v = static_cast<const uint8_t*>(p.v);
-  const int seq0 = p.cu[b];
-  const int len = p.cu[b + 1] - seq0;
-  const int m0 = mt * BM;
-  if (m0 >= len) return;
-  const int g = h / p.G;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int lq = lane & 31, hl = lane >> 5;
-  const int qi = m0 + w * 32 + lq;
-  const bool q_ok = qi < len;
-  const size_t kvrow = (size_t)p.Hkv * D * EB;   // bytes between consecutive keys
-  const uint8_t* kbase = k + ((size_t)seq0 * p.Hkv + g) * D * EB;
-  const uint8_t* vbase = v + ((size_t)seq0 * p.Hkv + g) * D * EB;
-
-  // ---- Q as the B operand of S^T = K Q^T
-  typedef typename std::conditional<FP8, i32x8, bf16x8>::type QOp;
-  QOp qreg[QKS];
-  {
-    const uint8_t* qr = q + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * D * EB;
-#pragma unroll
-    for (int ks = 0; ks < QKS; ++ks) {
-      if constexpr (FP8) {
-        const u32x4 lo = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl);
-        const u32x4 hi = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl + 16);
-        const i32x8 t = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                         (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-        qreg[ks] = __builtin_bit_cast(QOp, t);
-      } else {
-        qreg[ks] = __builtin_bit_cast(QOp, *reinterpret_cast<const u32x4*>(qr + (ks * 16 + 8 * hl) * 2));
-      }
-    }
-  }
-
-  f32x16 o[DB];
-#pragma unroll
-  for (int db = 0; db < DB; ++db)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-  const float c = p.scale_log2;
-
-  const int kend = CAUSAL ? min(len, m0 + BM) : len;
-  const int ntiles = (kend + BN - 1) / BN;
-  const int wave_q0 = m0 + w * 32;
-
-  // ---- tile loads: K pieces and V (key quad, head-dim chunk) pairs
-  u32x4 kreg[KPT];
-  typedef typename std::conditional<FP8, u32x2, u32x4>::type VLoad;
-  VLoad vreg[VPT][4];
-  auto fetch = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int pc = min(tid + 256 * i, KPIECES - 1);
-      const int key = pc / (D * EB / 16), off = (pc % (D * EB / 16)) * 16;
-      const int kk = min(k0 + key, len - 1);  // clamped; rows past len are zeroed on store
-      kreg[i] = *reinterpret_cast<const u32x4*>(kbase + kk * kvrow + off);
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int pr = min(tid + 256 * i, NPAIR - 1);
-      const int kq = pr / VCH, off = (pr % VCH) * VW;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const int kk = min(k0 + 4 * kq + u, len - 1);
-        vreg[i][u] = *reinterpret_cast<const VLoad*>(vbase + kk * kvrow + off);
-      }
-    }
-  };
-  auto store = [&](int buf, int k0) {
-#pragma unroll
-    for (int i = 0; i < KPT; ++i) {
-      const int pc = tid + 256 * i;
-      if (pc >= KPIECES) break;
-      const int key = pc / (D * EB / 16), off = (pc % (D * EB / 16)) * 16;
-      const u32x4 z = {0u, 0u, 0u, 0u};
-      *reinterpret_cast<u32x4*>(&Ks[buf][key * KROW + off]) = (k0 + key < len) ? kreg[i] : z;
-    }
-#pragma unroll
-    for (int i = 0; i < VPT; ++i) {
-      const int pr = tid + 256 * i;
-      if (pr >= NPAIR) break;
-      const int kq = pr / VCH, off = (pr % VCH) * VW;
-      // transpose: head dim d = off/EB + j gets the 4 keys 4kq..4kq+3
-#pragma unroll
-      for (int j = 0; j < VW / EB; ++j) {
-        uint32_t e[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          const bool ok = k0 + 4 * kq + u < len;
-          const uint32_t word = vreg[i][u][(j * EB) / 4];
-          const uint32_t sh = ((j * EB) % 4) * 8;
-          e[u] = ok ? (word >> sh) & (FP8 ? 0xFFu : 0xFFFFu) : 0u;
-        }
-        const int d = off / EB + j;
-        if constexpr (FP8) {
-          *reinterpret_cast<uint32_t*>(&Vt[buf][d * VROW + 4 * kq]) =
-              e[0] | (e[1] << 8) | (e[2] << 16) | (e[3] << 24);
-        } else {
-          const u32x2 pk = {e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
-          *reinterpret_cast<u32x2*>(&Vt[buf][d * VROW + 8 * kq]) = pk;
-        }
-      }
-    }
-  };
-
-  fetch(0);
-  store(0, 0);
-  __syncthreads();
-
-  for (int t = 0; t < ntiles; ++t) {
-    const int buf = t & 1;
-    const int k0 = t * BN;
-    if (t + 1 < ntiles) fetch(k0 + BN);
-    const bool active = !(CAUSAL && k0 > wave_q0 + 31);  // some key of the tile is visible
-    if (active) {
-      // ---- S^T blocks: 2 x (32 keys x 32 queries)
-      f32x16 s[2];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
-        const uint8_t* krow = &Ks[buf][tile_key<FP8>(nb, lq) * KROW];
-#pragma unroll
-        for (int ks = 0; ks < QKS; ++ks) {
-          if constexpr (FP8) {
-            const u32x4 lo = *reinterpret_cast<const u32x4*>(krow + ks * 64 + 32 * hl);
-            const u32x4 hi = *reinterpret_cast<const u32x4*>(krow + ks * 64 + 32 * hl + 16);
-            const i32x8 a = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                             (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-            s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(
-                a, __builtin_bit_cast(i32x8, qreg[ks]), s[nb], 0, 0, 0, 0, 0, 0);
-          } else {
-            const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(krow + (ks * 16 + 8 * hl) * 2));
-            s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, __builtin_bit_cast(bf16x8, qreg[ks]), s[nb], 0, 0, 0);
-          }
-        }
-      }
-      // ---- mask (edge tiles only) and tile max, in raw logit units
-      const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
-      if (need_mask) {
-#pragma unroll
-        for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + tile_key<FP8>(nb, acc_row32(r, hl));
-            if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
-          }
-      }
-      float mx = s[0][0];
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[nb][r]);
-      mx = max_xor32(mx);
-      // ---- lazy rescale
-      const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
-      if (__any(grow)) {
-        const float m_new = grow ? fmaxf(m_run, mx) : m_run;
-        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
-        m_run = m_new;
-      }
-      const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
-      // ---- P = exp2(s*c - m*c), row sums, MFMA operand
-      float rs = 0.f;
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float e = __builtin_amdgcn_exp2f(fmaf(s[nb][r], c, -mc));
-          s[nb][r] = e;
-          rs += e;
-        }
-      l_run += rs;
-      if constexpr (FP8) {
-        // byte s of the lane's 32-byte operand is key 32*hl + s: block s/16, register s%16
-        constexpr float PS = (float)(1 << PSHIFT);
-        int pw[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int nb = i >> 2, r0 = (i & 3) * 4;
-          int wd = __builtin_amdgcn_cvt_pk_fp8_f32(s[nb][r0] * PS, s[nb][r0 + 1] * PS, 0, false);
-          wd = __builtin_amdgcn_cvt_pk_fp8_f32(s[nb][r0 + 2] * PS, s[nb][r0 + 3] * PS, wd, true);
-          pw[i] = wd;
-        }
-        const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const uint8_t* vrow = &Vt[buf][(db * 32 + lq) * VROW + 32 * hl];
-          const u32x4 lo = *reinterpret_cast<const u32x4*>(vrow);
-          const u32x4 hi = *reinterpret_cast<const u32x4*>(vrow + 16);
-          const i32x8 a = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3],
-                           (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
-          o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, pb, o[db], 0, 0, 0, 0, 0, 0);
-        }
-      } else {
-        bf16x8 pb[4];
-#pragma unroll
-        for (int kk = 0; kk < 4; ++kk) {
-          const int nb = kk >> 1, r0 = 8 * (kk & 1);
-          pb[kk] = bf16x8{(__bf16)s[nb][r0], (__bf16)s[nb][r0 + 1], (__bf16)s[nb][r0 + 2],
-                          (__bf16)s[nb][r0 + 3], (__bf16)s[nb][r0 + 4], (__bf16)s[nb][r0 + 5],
-                          (__bf16)s[nb][r0 + 6], (__bf16)s[nb][r0 + 7]};
-        }
-#pragma unroll
-        for (int db = 0; db < DB; ++db) {
-          const uint8_t* vrow = &Vt[buf][(db * 32 + lq) * VROW + 16 * hl];
-#pragma unroll
-          for (int kk = 0; kk < 4; ++kk)
-            o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
-                __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(vrow + kk * 32)), pb[kk], o[db], 0, 0, 0);
-        }
-      }
-    }
-    if (t + 1 < ntiles) store(buf ^ 1, k0 + BN);
-    __syncthreads();
-  }
-
-  const float l = sum_xor32(l_run);
-  const float inv = (l > 0.f) ? p.out_scale / (l * (float)(1 << PSHIFT)) : 0.f;
-  if (q_ok) {
-    const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
-#pragma unroll
-    for (int db = 0; db < DB; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) store_out<OUT>(p.o, obase + db * 32 + acc_row32(r, hl), o[db][r] * inv);
-  }
-}
 
 // ---------------------------------------------------------------------------
 // bf16 path: 4 waves x 32 query rows of one head per workgroup, 64-key tiles
@@ -551,6 +284,217 @@ attn_bf16_kernel(AttnParams p) {
   }
 }
 
+// ---------------------------------------------------------------------------
+// E4M3 path: the bf16 kernel's structure on v_mfma_f32_32x32x64_f8f6f4. S^T
+// block nb holds keys 32*bit2(rho) + 16*nb + 4*(rho>>3) + (rho&3) in row rho, so
+// that a lane half's 32 accumulator values are keys 32*hl .. 32*hl+31, the B
+// operand of one P.V k-step. K rows are 16-byte pieces read directly; V is
+// row-major and read transposed with ds_read_b64_tr_b8 (8 keys per read).
+// P is quantised as p*2^8 under an exact running max.
+
+typedef int i32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
+
+template <int D, bool CAUSAL, int OUT>
+__global__ void __launch_bounds__(256, 2)
+attn_fp8_kernel(AttnParams p) {
+  constexpr int BN = 64, NW = 4, BM = 128;
+  constexpr int RB = D;                     // bytes per key row
+  constexpr int NP = RB / 16;               // 16-byte pieces per row
+  constexpr int TB = BN * RB;
+  constexpr int LI = (TB / 1024 + NW - 1) / NW;
+  constexpr int NI = TB / 1024;             // wave copies per tile
+  constexpr int QKS = D / 64, DB = D / 32;
+  constexpr int PSHIFT = 8;
+  static_assert(TB % 1024 == 0, "tile must split into whole wave copies");
+  __shared__ __attribute__((aligned(1024))) uint8_t Kl[2][TB];
+  __shared__ __attribute__((aligned(1024))) uint8_t Vl[2][TB];
+
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int m0 = mt * BM;
+  if (m0 >= len) return;
+  const int g = h / p.G;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lq = lane & 31, hl = lane >> 5;
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const uint32_t kvrow = (uint32_t)p.Hkv * RB;
+  const uint8_t* kbase = static_cast<const uint8_t*>(p.k) + ((size_t)seq0 * p.Hkv + g) * RB;
+  const uint8_t* vbase = static_cast<const uint8_t*>(p.v) + ((size_t)seq0 * p.Hkv + g) * RB;
+  const int qi = m0 + w * 32 + lq;
+  const int wave_q0 = m0 + w * 32;
+
+  // piece swizzles (involutions): K reads hit 16 rows x 1 piece per 16 lanes,
+  // V transposed reads 8 rows x 1 piece per 16 lanes
+  auto kswz = [](int r) {
+    return NP >= 8 ? (((r >> 1) & 3) | (((r >> 5) & 1) << 2)) : (((r >> 2) & 1) | (((r >> 5) & 1) << 1));
+  };
+  auto vswz = [](int r) { return (r >> 1) & (NP - 1) & 3; };
+
+  int ld_row[LI];
+  uint32_t ld_kpiece[LI], ld_vpiece[LI];
+#pragma unroll
+  for (int j = 0; j < LI; ++j) {
+    const int slot = min(w + NW * j, NI - 1) * 64 + lane;
+    const int r = slot / NP, ph = slot % NP;
+    ld_row[j] = r;
+    ld_kpiece[j] = (uint32_t)(ph ^ kswz(r)) * 16;
+    ld_vpiece[j] = (uint32_t)(ph ^ vswz(r)) * 16;
+  }
+  // K operand: rows tile_key<fp8>(nb, lq), pieces 4*ks + 2*hl and +1
+  uint32_t koff[2][QKS][2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) {
+    const int row = tile_key<true>(nb, lq);
+#pragma unroll
+    for (int ks = 0; ks < QKS; ++ks)
+#pragma unroll
+      for (int u = 0; u < 2; ++u) koff[nb][ks][u] = row * RB + (((4 * ks + 2 * hl + u) ^ kswz(row)) * 16);
+  }
+  // V operand: read j covers keys 32*(g16>>1) + 8*j + 0..7 at head dim 32*db + lq;
+  // source lane s16 addresses row 32*(g16>>1) + 8*j + (s16>>1), piece 2*db + (g16&1), half s16&1
+  uint32_t voff[DB];
+  const int vrow0 = 32 * (g16 >> 1) + (s16 >> 1);
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+    voff[db] = vrow0 * RB + (((2 * db + (g16 & 1)) ^ vswz(vrow0)) * 16) + (s16 & 1) * 8;
+  // rows vrow0 + 8*j share vswz: (r>>1)&3 depends on bits 1,2 only
+
+  auto copy_tile = [&](int tile, int buf) {
+    const int k0 = tile * BN;
+    const bool full = k0 + BN <= len;
+#pragma unroll
+    for (int j = 0; j < LI; ++j) {
+      if (w + NW * j >= NI) break;
+      const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
+      const uint32_t ro = (uint32_t)key * kvrow;
+      __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
+                                       (__attribute__((address_space(3))) void*)(&Kl[buf][(w + NW * j) * 1024]),
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
+                                       (__attribute__((address_space(3))) void*)(&Vl[buf][(w + NW * j) * 1024]),
+                                       16, 0, 0);
+    }
+  };
+
+  i32x8 qreg[QKS];
+  {
+    const uint8_t* qr = static_cast<const uint8_t*>(p.q) + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * RB;
+#pragma unroll
+    for (int ks = 0; ks < QKS; ++ks) {
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(qr + ks * 64 + 32 * hl + 16);
+      qreg[ks] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+    }
+  }
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = p.scale_log2;
+  const int kend = CAUSAL ? min(len, m0 + BM) : len;
+  const int nt = (kend + BN - 1) / BN;
+
+  copy_tile(0, 0);
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  for (int t = 0; t < nt; ++t) {
+    const int buf = t & 1;
+    const int k0 = t * BN;
+    if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);
+    if (!(CAUSAL && k0 > wave_q0 + 31)) {
+      const uint8_t* kl = Kl[buf];
+      f32x16 s[2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+#pragma unroll
+      for (int ks = 0; ks < QKS; ++ks) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          const u32x4 lo = *reinterpret_cast<const u32x4*>(kl + koff[nb][ks][0]);
+          const u32x4 hi = *reinterpret_cast<const u32x4*>(kl + koff[nb][ks][1]);
+          const i32x8 a = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+          s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, qreg[ks], s[nb], 0, 0, 0, 0, 0, 0);
+        }
+      }
+      const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
+      if (need_mask) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + tile_key<true>(nb, acc_row32(r, hl));
+            if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
+          }
+      }
+      float mx = fmaxf(s[0][0], s[1][0]);
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
+      mx = max_xor32(mx);
+      // exact running max: rescale whenever it grows
+      const bool grow = mx > m_run;
+      if (__any(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        m_run = m_new;
+      }
+      // p * 2^PSHIFT = exp2(s*c - m*c + PSHIFT)
+      const float mc = (m_run == -INFINITY) ? 0.f : m_run * c - (float)PSHIFT;
+      float rs = 0.f;
+      int pw[8];
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int nb = i >> 2, r0 = (i & 3) * 4;
+        float e[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          e[u] = __builtin_amdgcn_exp2f(fmaf(s[nb][r0 + u], c, -mc));
+          rs += e[u];
+        }
+        int wd = __builtin_amdgcn_cvt_pk_fp8_f32(e[0], e[1], 0, false);
+        pw[i] = __builtin_amdgcn_cvt_pk_fp8_f32(e[2], e[3], wd, true);
+      }
+      l_run += rs;
+      const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
+      const uint8_t* vl = Vl[buf];
+#pragma unroll
+      for (int db = 0; db < DB; ++db) {
+        i32x2 part[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          part[j] = __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2*)(vl + voff[db] + (8 * j) * RB));
+        const i32x8 va = {part[0][0], part[0][1], part[1][0], part[1][1],
+                          part[2][0], part[2][1], part[3][0], part[3][1]};
+        o[db] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(va, pb, o[db], 0, 0, 0, 0, 0, 0);
+      }
+    }
+    wait_vmcnt<0>();
+    __syncthreads();
+  }
+
+  const float l = sum_xor32(l_run);
+  const float inv = (l > 0.f) ? p.out_scale / l : 0.f;   // l already carries 2^PSHIFT
+  if (qi < len) {
+    const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) store_out<OUT>(p.o, obase + db * 32 + acc_row32(r, hl), o[db][r] * inv);
+  }
+}
+
 // fp32 path: one lane per query row, K/V tiles of 64 keys staged in LDS,
 // plain FMAs. Meant for small fp32 problems.
 template <int D, bool CAUSAL, int OUT>
@@ -624,7 +568,7 @@ static void launch_typed(const AttnArgs& a, AttnParams& p, hipStream_t stream) {
   if (a.in_dtype == LITEVLM_BF16)
     hipLaunchKernelGGL((attn_bf16_kernel<D, CAUSAL, OUT>), grid, dim3(256), 0, stream, p);
   else if (a.in_dtype == LITEVLM_FP8_E4M3)
-    hipLaunchKernelGGL((attn_fwd_kernel<D, CAUSAL, OUT, true>), grid, dim3(256), 0, stream, p);
+    hipLaunchKernelGGL((attn_fp8_kernel<D, CAUSAL, OUT>), grid, dim3(256), 0, stream, p);
   else
     hipLaunchKernelGGL((attn_fwd_f32_kernel<D, CAUSAL, OUT>), grid, dim3(64), 0, stream, p);
 }
