@@ -143,7 +143,9 @@ size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full,
  *   qc, kc, vc         dev out packed rows of Q, K, V at kept_index, capacity B*S
  *                      rows of Hq*D / Hkv*D / Hkv*D elements, exact copies of the
  *                      input bits; each may be NULL to skip that copy
- *   workspace          dev scratch of litevlm_token_score_topk_workspace() bytes
+ *   workspace          dev scratch of litevlm_token_score_topk_workspace() bytes;
+ *                      its contents on entry are ignored, and calls that may run
+ *                      concurrently must not share one workspace
  */
 litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
                                           int32_t Hq, int32_t Hkv, int32_t D,

@@ -110,8 +110,11 @@ attn_bf16_kernel(AttnParams p) {
   // V swizzle: piece ^ 4*(row & 3) keeps the 4 rows x 4 pieces of a transposed
   // read distinct (D = 64 has only 8 pieces per row: piece ^ 4*(row & 1)).
   constexpr int VSW = NP >= 16 ? 3 : 1;
-  __shared__ __attribute__((aligned(1024))) uint8_t Kl[2][TB];
-  __shared__ __attribute__((aligned(1024))) uint8_t Vl[2][TB];
+  // One LDS object holds both K and V double buffers (K at buf*TB, V at
+  // (2+buf)*TB). With a single object the compiler adds no vmcnt wait of its
+  // own between a direct copy into one buffer and reads of the other; the
+  // explicit wait + barrier below orders each buffer's copy before its reads.
+  __shared__ __attribute__((aligned(1024))) uint8_t kvl[4 * TB];
 
   int b, h, mt;
   if (!decode_work(p, b, h, mt)) return;
@@ -165,10 +168,10 @@ attn_bf16_kernel(AttnParams p) {
       const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
       const uint32_t ro = (uint32_t)key * kvrow;
       __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(&Kl[buf][(w + NW * j) * 1024]),
+                                       (__attribute__((address_space(3))) void*)(kvl + buf * TB + (w + NW * j) * 1024),
                                        16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(&Vl[buf][(w + NW * j) * 1024]),
+                                       (__attribute__((address_space(3))) void*)(kvl + (2 + buf) * TB + (w + NW * j) * 1024),
                                        16, 0, 0);
     }
   };
@@ -200,7 +203,7 @@ attn_bf16_kernel(AttnParams p) {
     if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);   // buffer last read in step t-1
     if (!(CAUSAL && k0 > wave_q0 + 31)) {
       // ---- S^T blocks: 2 x (32 keys x 32 queries)
-      const uint8_t* kl = Kl[buf];
+      const uint8_t* kl = kvl + buf * TB;
       f32x16 s[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -257,7 +260,7 @@ attn_bf16_kernel(AttnParams p) {
                         (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
       }
       l_run += rs;
-      const uint8_t* vl = Vl[buf];
+      const uint8_t* vl = kvl + (2 + buf) * TB;
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
 #pragma unroll
@@ -307,8 +310,11 @@ attn_fp8_kernel(AttnParams p) {
   constexpr int QKS = D / 64, DB = D / 32;
   constexpr int PSHIFT = 8;
   static_assert(TB % 1024 == 0, "tile must split into whole wave copies");
-  __shared__ __attribute__((aligned(1024))) uint8_t Kl[2][TB];
-  __shared__ __attribute__((aligned(1024))) uint8_t Vl[2][TB];
+  // One LDS object holds both K and V double buffers (K at buf*TB, V at
+  // (2+buf)*TB). With a single object the compiler adds no vmcnt wait of its
+  // own between a direct copy into one buffer and reads of the other; the
+  // explicit wait + barrier below orders each buffer's copy before its reads.
+  __shared__ __attribute__((aligned(1024))) uint8_t kvl[4 * TB];
 
   int b, h, mt;
   if (!decode_work(p, b, h, mt)) return;
@@ -371,10 +377,10 @@ attn_fp8_kernel(AttnParams p) {
       const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
       const uint32_t ro = (uint32_t)key * kvrow;
       __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(&Kl[buf][(w + NW * j) * 1024]),
+                                       (__attribute__((address_space(3))) void*)(kvl + buf * TB + (w + NW * j) * 1024),
                                        16, 0, 0);
       __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(&Vl[buf][(w + NW * j) * 1024]),
+                                       (__attribute__((address_space(3))) void*)(kvl + (2 + buf) * TB + (w + NW * j) * 1024),
                                        16, 0, 0);
     }
   };
@@ -408,7 +414,7 @@ attn_fp8_kernel(AttnParams p) {
     const int k0 = t * BN;
     if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);
     if (!(CAUSAL && k0 > wave_q0 + 31)) {
-      const uint8_t* kl = Kl[buf];
+      const uint8_t* kl = kvl + buf * TB;
       f32x16 s[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -468,7 +474,7 @@ attn_fp8_kernel(AttnParams p) {
       }
       l_run += rs;
       const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
-      const uint8_t* vl = Vl[buf];
+      const uint8_t* vl = kvl + (2 + buf) * TB;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         i32x2 part[4];

@@ -18,8 +18,8 @@ hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const
                                const float* lexical, float w, float tau, uint8_t* view_keep,
                                uint8_t* token_keep, int32_t* n_visual_kept, hipStream_t stream);
 
-// Keys per workgroup of the two scoring sweeps (4 waves x 32 keys).
-constexpr int kScoreKeyTile = 128;
+// Keys per workgroup of the two scoring sweeps (4 waves x 64 keys).
+constexpr int kScoreKeyTile = 256;
 
 // Row-chunk split of the two sweeps over workgroups (a function of the shape
 // only, so that the workspace size is too).

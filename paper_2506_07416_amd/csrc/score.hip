@@ -10,344 +10,438 @@
 //   sweep 1  per (key tile, row): max m and sum Z of exp2(logit) over the tile
 //   merge    per row: m = max over tiles, Z = sum Z_tile * exp2(m_tile - m)
 //   sweep 2  per visual key: sum over rows of exp2(logit - m) / Z
-// Logits are formed transposed, S^T = K Q^T, on MFMA: the key tile stays in
-// registers as the A operand and 16 query rows at a time stream through the B
-// operand. In the 16x16 accumulator a lane owns one query row (lane % 16) and
-// four keys per 16-key block (4*(lane/16) + e). Every reduction runs in a
-// fixed order, so results are deterministic.
+// Logits are formed transposed, S^T = K Q^T, on 32x32 MFMAs: a wave's 64 keys
+// stay in registers as the A operand and 32 query rows at a time stream
+// through the B operand from LDS. In the 32x32 accumulator a lane owns one
+// query row (lane % 32) and 16 keys per 32-key block. Every reduction runs in
+// a fixed order, so results are deterministic.
 #include <algorithm>
-#include <climits>
+#include <type_traits>
 
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace litevlm {
 
-constexpr int KW = 32;             // keys per wave: 2 blocks of 16
+constexpr int KW = 64;                    // keys per wave: 2 blocks of 32
 constexpr int kScoreWaves = 4;
-constexpr int KT = KW * kScoreWaves;  // keys per workgroup
+constexpr int KT = KW * kScoreWaves;      // keys per workgroup
+constexpr int CH = 32;                    // text rows per chunk
+constexpr int PMAX = 8;                   // chunks whose row statistics are combined at once
 static_assert(KT == kScoreKeyTile, "workspace layout and kernels disagree on the key tile");
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+struct ScoreDims {
+  int B, S, V_full, T, Hq, Hkv, G, R, nchunks;
+  int n_kt, n_vt, rs1, rs2;
+  float scale_log2;
+};
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
+}
+
+// Flat, XCD-aware work decode. Workgroup L runs on XCD L % 8; XCD x takes the
+// contiguous column range [x*ncol/8, (x+1)*ncol/8), every column with all of
+// its row splits, so a key tile and its KV group's query rows are read into
+// one XCD's L2. Returns false for the padding workgroups of the grid.
+__device__ __forceinline__ bool decode_column(int ncol, int nsplit, int& col, int& split) {
+  const int L = blockIdx.x, x = L & 7, j = L >> 3;
+  const int c0 = (int)(((long long)x * ncol) >> 3), c1 = (int)(((long long)(x + 1) * ncol) >> 3);
+  if (j >= (c1 - c0) * nsplit) return false;
+  const int cj = j / nsplit;
+  col = c0 + cj;
+  split = j - cj * nsplit;
+  return true;
+}
+
 // ---------------------------------------------------------------- logit tiles
-// Each tile policy holds one wave's 32 keys of one KV head and produces, for
-// the 16 query rows of a chunk staged in LDS,
-//   acc[kb][e] = k(kb*16 + 4*(lane/16) + e) . q(lane % 16)   in fp32.
+// A tile policy holds one wave's 64 keys of one KV head in registers (the A
+// operand of S^T = K Q^T) and forms, for the 32 query rows of a chunk staged
+// in LDS, s[nb][r] = k(32*nb + acc_row(r)) . q(lane % 32) in fp32, with
+// acc_row(r) = 8*(r/4) + 4*(lane/32) + r%4, the 32x32 accumulator layout.
+// ro[] are the lane's byte offsets of its B-operand pieces within a chunk.
+
+__device__ __forceinline__ int acc_row(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
 
 template <int D>
 struct TileBf16 {
-  static constexpr int KS = D / 32;  // k-steps of v_mfma_f32_16x16x32_bf16
-  static constexpr int ROW_BYTES = D * 2;
+  static constexpr int RB = D * 2;        // bytes per row
+  static constexpr int NP = RB / 16;      // 16-byte pieces per row
+  static constexpr int KS = D / 16;       // k-steps of v_mfma_f32_32x32x16_bf16
   bf16x8 kreg[2][KS];
+  uint32_t ro[KS];
+  // LDS piece swizzle of Q rows: each 16-lane group reads 16 rows x 1 piece
+  __device__ __forceinline__ static int qswz(int r) { return r & (NP - 1); }
 
-  __device__ __forceinline__ void load_keys(const uint16_t* kbase, size_t kstride, int nvalid,
-                                            int lane) {
-    const int c = lane & 15, g4 = lane >> 4;
+  __device__ __forceinline__ void init(int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int key = kb * 16 + c;
+    for (int ks = 0; ks < KS; ++ks) ro[ks] = lq * RB + ((2 * ks + hl) ^ qswz(lq)) * 16;
+  }
+
+  __device__ __forceinline__ void load_keys(const uint8_t* kbase, size_t kstride, int nvalid, int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int key = min(nb * 32 + lq, max(nvalid - 1, 0));
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks)
-        kreg[kb][ks] = key < nvalid
-            ? *reinterpret_cast<const bf16x8*>(kbase + key * kstride + ks * 32 + 8 * g4)
-            : bf16x8{};
+        kreg[nb][ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(
+                                                      kbase + key * kstride + (ks * 16 + 8 * hl) * 2));
     }
   }
 
-  // qrow: LDS address of this lane's query row (row lane % 16 of the chunk).
-  __device__ __forceinline__ void logits(const uint8_t* qrow, int lane, f32x4 acc[2]) const {
-    const int g4 = lane >> 4;
-    bf16x8 qreg[KS];
+  __device__ __forceinline__ void logits(const uint8_t* buf, int, f32x16 s[2]) const {
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = *reinterpret_cast<const bf16x8*>(qrow + (ks * 32 + 8 * g4) * 2);
+    for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x4 a = {0.f, 0.f, 0.f, 0.f};
+      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
 #pragma unroll
-      for (int ks = 0; ks < KS; ++ks)
-        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kreg[kb][ks], qreg[ks], a, 0, 0, 0);
-      acc[kb] = a;
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 qb = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + ro[ks]));
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[nb][ks], qb, s[nb], 0, 0, 0);
     }
   }
 };
 
 template <int D>
 struct TileFp8 {
-  // v_mfma_f32_16x16x128_f8f6f4: one k-step covers 128 head dims; a lane
-  // supplies 32 consecutive E4M3 bytes. D = 64 zero-pads the upper half.
-  static constexpr int ROW_BYTES = D;
-  i32x8 kreg[2];
+  // v_mfma_f32_32x32x64_f8f6f4: a lane supplies 32 consecutive E4M3 bytes per k-step
+  static constexpr int RB = D;
+  static constexpr int NP = RB / 16;
+  static constexpr int KS = D / 64;
+  i32x8 kreg[2][KS];
+  uint32_t ro[2 * KS];
+  __device__ __forceinline__ static int qswz(int r) { return (r >> 1) & (NP - 1); }
 
-  __device__ __forceinline__ void load_keys(const uint8_t* kbase, size_t kstride, int nvalid,
-                                            int lane) {
-    const int c = lane & 15, g4 = lane >> 4;
+  __device__ __forceinline__ void init(int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const int key = kb * 16 + c;
-      kreg[kb] = (key < nvalid && 32 * g4 < D)
-          ? *reinterpret_cast<const i32x8*>(kbase + key * kstride + 32 * g4)
-          : i32x8{};
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int hp = 0; hp < 2; ++hp) ro[2 * ks + hp] = lq * RB + ((4 * ks + 2 * hl + hp) ^ qswz(lq)) * 16;
+  }
+
+  __device__ __forceinline__ void load_keys(const uint8_t* kbase, size_t kstride, int nvalid, int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int key = min(nb * 32 + lq, max(nvalid - 1, 0));
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const uint8_t* p = kbase + key * kstride + ks * 64 + 32 * hl;
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(p);
+        const u32x4 hi = *reinterpret_cast<const u32x4*>(p + 16);
+        kreg[nb][ks] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+      }
     }
   }
 
-  __device__ __forceinline__ void logits(const uint8_t* qrow, int lane, f32x4 acc[2]) const {
-    const int g4 = lane >> 4;
-    i32x8 qreg = i32x8{};
-    if (32 * g4 < D) {
-      const i32x4 lo = *reinterpret_cast<const i32x4*>(qrow + 32 * g4);
-      const i32x4 hi = *reinterpret_cast<const i32x4*>(qrow + 32 * g4 + 16);
-      qreg = i32x8{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
-    }
+  __device__ __forceinline__ void logits(const uint8_t* buf, int, f32x16 s[2]) const {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-      // format 0 = E4M3 for both operands; zero scale operands select the
-      // unscaled instruction.
-      acc[kb] = __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(kreg[kb], qreg, z, 0, 0, 0, 0, 0, 0);
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(buf + ro[2 * ks]);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(buf + ro[2 * ks + 1]);
+      const i32x8 qb = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        // format 0 = E4M3 for both operands; zero scale operands select the unscaled instruction
+        s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kreg[nb][ks], qb, s[nb], 0, 0, 0, 0, 0, 0);
     }
   }
 };
 
 template <int D>
 struct TileF32 {
-  // Plain fp32 FMAs; fp32 inputs are only used at small sizes. The lane's own
-  // 8 keys are read from global memory, its query row from LDS.
-  static constexpr int ROW_BYTES = D * 4;
-  const float* kbase;
+  // Plain fp32 FMAs; fp32 inputs are only used at small sizes. The lane's 32
+  // accumulator keys are read from global memory, its query row from LDS.
+  static constexpr int RB = D * 4;
+  static constexpr int NP = RB / 16;
+  const uint8_t* kbase;
   size_t kstride;
   int nvalid;
+  __device__ __forceinline__ static int qswz(int) { return 0; }
+  __device__ __forceinline__ void init(int) {}
 
-  __device__ __forceinline__ void load_keys(const float* kb_, size_t ks_, int nv, int) {
+  __device__ __forceinline__ void load_keys(const uint8_t* kb_, size_t ks_, int nv, int) {
     kbase = kb_;
     kstride = ks_;
     nvalid = nv;
   }
 
-  __device__ __forceinline__ void logits(const uint8_t* qrow, int lane, f32x4 acc[2]) const {
-    const int g4 = lane >> 4;
-    const float* qf = reinterpret_cast<const float*>(qrow);
+  __device__ __forceinline__ void logits(const uint8_t* buf, int lane, f32x16 s[2]) const {
+    const int lq = lane & 31, hl = lane >> 5;
+    const float* qf = reinterpret_cast<const float*>(buf + lq * RB);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = kb * 16 + 4 * g4 + e;
-        float s = 0.f;
+    for (int nb = 0; nb < 2; ++nb)
+      for (int r = 0; r < 16; ++r) {
+        const int key = nb * 32 + acc_row(r, hl);
+        float acc = 0.f;
         if (key < nvalid) {
-          const float* kr = kbase + key * kstride;
-          for (int d = 0; d < D; ++d) s = fmaf(qf[d], kr[d], s);
+          const float* kr = reinterpret_cast<const float*>(kbase + key * kstride);
+          for (int dd = 0; dd < D; ++dd) acc = fmaf(qf[dd], kr[dd], acc);
         }
-        acc[kb][e] = s;
+        s[nb][r] = acc;
       }
-    }
   }
 };
 
 template <int DT, int D>
 struct TileOf;
-template <int D> struct TileOf<LITEVLM_BF16, D> { using T = TileBf16<D>; using E = uint16_t; };
-template <int D> struct TileOf<LITEVLM_FP8_E4M3, D> { using T = TileFp8<D>; using E = uint8_t; };
-template <int D> struct TileOf<LITEVLM_F32, D> { using T = TileF32<D>; using E = float; };
+template <int D> struct TileOf<LITEVLM_BF16, D> { using T = TileBf16<D>; };
+template <int D> struct TileOf<LITEVLM_FP8_E4M3, D> { using T = TileFp8<D>; };
+template <int D> struct TileOf<LITEVLM_F32, D> { using T = TileF32<D>; };
 
-struct ScoreDims {
-  int S, V_full, T, Hq, Hkv, G, R, n_kt, rs1, rs2;
-  float scale_log2;
-};
+// Text query rows of a workgroup pass through two chunk buffers in LDS,
+// filled with direct global -> LDS copies (16-byte pieces, XOR-swizzled per
+// row) two chunks ahead of use. Row r of KV group g is query head g*G + r%G
+// of text token r/G; each lane tracks (token, head) of its copies and steps
+// them by the row distance between the workgroup's chunks. Rows past R repeat
+// a valid row; callers ignore them.
+template <class Tile>
+struct QRing {
+  static constexpr int RB = Tile::RB;
+  static constexpr int NP = Tile::NP;
+  static constexpr int CB = CH * RB;                            // bytes per chunk
+  static constexpr int IPC = CB / 1024;                         // wave copies per chunk
+  static constexpr int CPW = (IPC + kScoreWaves - 1) / kScoreWaves;
+  static constexpr int BYTES = 2 * CB;
+  static_assert(CB % 1024 == 0, "a chunk must split into whole wave copies");
+  static_assert(IPC % kScoreWaves == 0 || IPC < kScoreWaves, "copies must split evenly over waves");
 
-// Keep flags of the lane's 8 accumulator keys (bit kb*4+e): all 8 byte loads
-// are issued from clamped addresses before any is used.
-__device__ __forceinline__ uint32_t lane_keep_bits(const uint8_t* keep_row, int key0, int S, int lane) {
-  if (keep_row == nullptr) return 0xFFu;
-  const int g4 = lane >> 4;
-  uint8_t f[8];
-#pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) f[kb * 4 + e] = keep_row[min(key0 + kb * 16 + 4 * g4 + e, S - 1)];
-  uint32_t m = 0;
-#pragma unroll
-  for (int i = 0; i < 8; ++i) m |= (f[i] ? 1u : 0u) << i;
-  return m;
-}
+  const uint8_t* qbase;  // row (text token 0, head g*G) of this sample and group
+  int G, Hq, T, dt, dh;
+  int t[CPW], hh[CPW];
+  uint32_t src[CPW];     // byte offset of the lane's piece within its row
 
-// Bitmask over the lane's 8 accumulator keys (bit kb*4+e): key is visual and kept.
-__device__ __forceinline__ uint32_t kept_visual_mask(const uint8_t* keep_row, int key0, int V_full,
-                                                     int S, int lane) {
-  const int g4 = lane >> 4;
-  const uint32_t kf = lane_keep_bits(keep_row, key0, S, lane);
-  uint32_t m = 0;
+  __device__ __forceinline__ void init(const uint8_t* q, int b, int g, const ScoreDims& d, int w, int lane,
+                                       int row0, int cstep) {
+    qbase = q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * RB;
+    G = d.G;
+    Hq = d.Hq;
+    T = d.T;
+    dt = cstep / d.G;
+    dh = cstep - dt * d.G;
 #pragma unroll
-  for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int i = kb * 4 + e;
-      const int key = key0 + kb * 16 + 4 * g4 + e;
-      if (key < V_full && ((kf >> i) & 1u)) m |= 1u << i;
+    for (int j = 0; j < CPW; ++j) {
+      const int slot = (w + kScoreWaves * j) * 64 + lane;
+      const int row = slot / NP;
+      src[j] = ((slot % NP) ^ Tile::qswz(row)) * 16;
+      const int r = row0 + row;
+      t[j] = r / G;
+      hh[j] = r - t[j] * G;
     }
-  return m;
-}
+  }
 
-// Byte address of text query row r of KV group g: query head g*G + r%G of text token r/G.
-__device__ __forceinline__ const uint8_t* text_row(const uint8_t* q, int b, int g, int r,
-                                                   const ScoreDims& d, int row_bytes) {
-  const int t = r / d.G, hh = r - t * d.G;
-  return q + (((size_t)b * d.S + d.V_full + t) * d.Hq + (size_t)g * d.G + hh) * row_bytes;
-}
-
-// Q rows of the workgroup, staged through LDS a block of up to kQBlockBytes
-// at a time: every load of a block is issued before the first is waited on.
-constexpr int kQBlockBytes = 70 * 1024;  // 16 chunks of 16 bf16 D=128 rows
-
-template <int ROW_BYTES>
-struct QBlock {
-  static constexpr int VEC = ROW_BYTES / 16;     // 16-byte pieces per row
-  static constexpr int STRIDE = ROW_BYTES + 16;  // padded LDS row
-  static constexpr int CHUNKS = kQBlockBytes / (16 * STRIDE) > 0 ? kQBlockBytes / (16 * STRIDE) : 1;
-  static constexpr int BYTES = CHUNKS * 16 * STRIDE;
-
-  static constexpr int PPT = (CHUNKS * 16 * VEC + 255) / 256;  // pieces per thread
-
-  // Stage chunks first, first+step, ... (at most CHUNKS of them, all < nchunks)
-  // into lds; returns how many were staged. Loads use clamped, always-valid
-  // addresses and are all issued before the first store.
-  __device__ __forceinline__ static int stage(uint8_t* lds, const uint8_t* q, int b, int g, int first,
-                                              int step, int nchunks, const ScoreDims& d) {
-    const int n = min(CHUNKS, (nchunks - first + step - 1) / step);
-    const int pieces = n * 16 * VEC;
-    uint4 reg[PPT];
+  // copies of the current chunk into buf, then step to the workgroup's next chunk
+  __device__ __forceinline__ void issue(uint8_t* buf, int w) {
 #pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int v = min((int)threadIdx.x + 256 * j, pieces - 1);
-      const int row = v / VEC, piece = v - row * VEC;  // row within the staged block
-      const int r = min((first + (row >> 4) * step) * 16 + (row & 15), d.R - 1);
-      reg[j] = *reinterpret_cast<const uint4*>(text_row(q, b, g, r, d, ROW_BYTES) + piece * 16);
+    for (int j = 0; j < CPW; ++j) {
+      const int sub = w + kScoreWaves * j;
+      if (sub < IPC) {
+        const int tt = min(t[j], T - 1);
+        __builtin_amdgcn_global_load_lds((const void*)(qbase + ((size_t)tt * Hq + hh[j]) * RB + src[j]),
+                                         (__attribute__((address_space(3))) void*)(buf + sub * 1024),
+                                         16, 0, 0);
+      }
+      hh[j] += dh;
+      t[j] += dt;
+      if (hh[j] >= G) {
+        hh[j] -= G;
+        t[j] += 1;
+      }
     }
-#pragma unroll
-    for (int j = 0; j < PPT; ++j) {
-      const int v = threadIdx.x + 256 * j;
-      const int row = v / VEC, piece = v - row * VEC;
-      const int r = (first + (row >> 4) * step) * 16 + (row & 15);
-      if (v < pieces)
-        *reinterpret_cast<uint4*>(lds + row * STRIDE + piece * 16) =
-            r < d.R ? reg[j] : make_uint4(0, 0, 0, 0);
-    }
-    return n;
   }
 };
 
+// True on every lane when all 64 keys of the wave are kept visual keys.
+__device__ __forceinline__ bool wave_all_visible(const uint8_t* keep_row, int key0, int V_full, int S, int lane) {
+  const int key = key0 + lane;
+  const uint8_t f = keep_row ? keep_row[min(key, S - 1)] : 1;
+  return __ballot(key < V_full && f) == ~0ull;
+}
+
+// Workgroup-wide OR through four per-wave words of the kernel's own LDS
+// array (the runtime's block reduction would add an LDS object of its own).
+__device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
+  const uint64_t m = __ballot(v);
+  if ((threadIdx.x & 63) == 0) slots[threadIdx.x >> 6] = m != 0;
+  __syncthreads();
+  const bool r = (slots[0] | slots[1] | slots[2] | slots[3]) != 0;
+  __syncthreads();
+  return r;
+}
+
+// Bit j (j = 16*nb + r) of the lane's 32 accumulator keys key0 + 32*nb +
+// acc_row(r, lane/32) set where key < limit and kept. Keys ascend with j.
+__device__ __forceinline__ uint32_t lane_key_bits(const uint8_t* keep_row, int key0, int limit, int S,
+                                                  int lane) {
+  const int hl = lane >> 5;
+  uint32_t m = 0;
+  if (keep_row) {
+    uint8_t f[32];
+#pragma unroll
+    for (int j = 0; j < 32; ++j) f[j] = keep_row[min(key0 + (j >> 4) * 32 + acc_row(j & 15, hl), S - 1)];
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+      m |= (uint32_t)((key0 + (j >> 4) * 32 + acc_row(j & 15, hl) < limit) & (f[j] != 0)) << j;
+  } else {
+#pragma unroll
+    for (int j = 0; j < 32; ++j) m |= (uint32_t)(key0 + (j >> 4) * 32 + acc_row(j & 15, hl) < limit) << j;
+  }
+  return m;
+}
+
+// Number of the lane's 32 accumulator keys that are <= key0 + 4*(lane/32) + L;
+// they form a prefix of the bit order above.
+__device__ __forceinline__ int keys_upto(int L) {
+  int n = 0;
+#pragma unroll
+  for (int q4 = 0; q4 < 8; ++q4) n += min(max(L - 8 * q4 + 1, 0), 4);  // quad q4 holds offsets 8*q4 + 0..3
+  return n;
+}
+
 // ---------------------------------------------------------------- sweep 1
-// grid (n_kt, Hkv, B*rs1). Wave w holds keys [kt*128 + 32w, +32). Every wave
-// runs over the workgroup's row chunks (chunk = rs, rs + rs1, ...); the four
-// waves' per-row (max, sum) are combined in LDS in wave order.
+// Flat grid over columns (b, g, key tile kt) x rs1 row splits. Wave w holds
+// keys [kt*256 + 64w, +64); the workgroup runs over its row chunks (chunk =
+// split, split + rs1, ...). Per chunk each wave forms its 64 x 32 logits and
+// the per-row (max, sum) over its keys; every PMAX chunks the four waves'
+// statistics are combined in wave order and written to rowpart.
 
 template <int DT, int D>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, 4)
 score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                       const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
   using Tile = typename TileOf<DT, D>::T;
-  using E = typename TileOf<DT, D>::E;
-  using QB = QBlock<Tile::ROW_BYTES>;
-  __shared__ __attribute__((aligned(16))) uint8_t qlds[QB::BYTES];
-  __shared__ float2 part[QB::CHUNKS][kScoreWaves][16];
+  using Ring = QRing<Tile>;
+  // One LDS object (the Q ring, then the per-wave row statistics): with a
+  // single object the compiler adds no vmcnt wait of its own before reads of
+  // one ring buffer while direct copies into the other are in flight; the
+  // explicit wait + barrier at each chunk orders copies before reads.
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES + PMAX * kScoreWaves * CH * sizeof(float2)];
+  float2 (*part)[kScoreWaves][CH] = reinterpret_cast<float2 (*)[kScoreWaves][CH]>(lds + Ring::BYTES);
 
+  int col, rs;
+  if (!decode_column(d.B * d.Hkv * d.n_kt, d.rs1, col, rs)) return;
+  const int bg = col / d.n_kt, kt = col - bg * d.n_kt;
+  const int b = bg / d.Hkv, g = bg - b * d.Hkv;
   const uint8_t* q = static_cast<const uint8_t*>(qv);
-  const E* k = static_cast<const E*>(kv);
-  const int kt = blockIdx.x, g = blockIdx.y;
-  const int b = blockIdx.z / d.rs1, rs = blockIdx.z - b * d.rs1;
+  const uint8_t* k = static_cast<const uint8_t*>(kv);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = lane & 15, g4 = lane >> 4;
+  const int lq = lane & 31, hl = lane >> 5;
   const int key0 = kt * KT + w * KW;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
-  const int nchunks = (d.R + 15) / 16;
+  const int nch = (d.nchunks - rs + d.rs1 - 1) / d.rs1;  // chunks rs, rs + rs1, ...
+  const int cstep = d.rs1 * CH;                          // rows between them
+  const int row0 = rs * CH;
   float2* out = rowpart + (((size_t)b * d.Hkv + g) * d.n_kt + kt) * d.R;
 
   // A tile of dropped-view keys only (no text key) contributes (-inf, 0).
-  bool any = false;
-  if (tid < KT) {
-    const int key = kt * KT + tid;
-    any = key < d.S && (key >= d.V_full || keep_row == nullptr || keep_row[key]);
-  }
-  if (!__syncthreads_or(any)) {
-    for (int ch = rs; ch < nchunks; ch += d.rs1)
-      if (tid < 16 && ch * 16 + tid < d.R) out[ch * 16 + tid] = make_float2(-INFINITY, 0.f);
-    return;
-  }
-
-  Tile tile;
-  tile.load_keys(k + (((size_t)b * d.S + min(key0, d.S)) * d.Hkv + g) * D, (size_t)d.Hkv * D,
-                 max(0, min(KW, d.S - key0)), lane);
-  // Per accumulator key: visible to text token t iff t >= lim (kept visual
-  // keys: -1; text key V_full+t': t'; dropped or past the end: never).
-  int lim[8];
-  bool need_mask = false;
   {
-    const uint32_t vis = kept_visual_mask(keep_row, key0, d.V_full, d.S, lane);
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int i = kb * 4 + e;
-        const int key = key0 + kb * 16 + 4 * g4 + e;
-        int l;
-        if (key >= d.S) l = INT_MAX;
-        else if (key >= d.V_full) l = key - d.V_full;
-        else l = ((vis >> i) & 1u) ? -1 : INT_MAX;
-        lim[i] = l;
-        need_mask |= l != -1;
-      }
-  }
-  need_mask = __any(need_mask);
-  const float sc = d.scale_log2;
-
-  for (int first = rs; first < nchunks; first += d.rs1 * QB::CHUNKS) {
-    const int n = QB::stage(qlds, q, b, g, first, d.rs1, nchunks, d);
-    __syncthreads();
-    for (int i = 0; i < n; ++i) {
-      const int r = (first + i * d.rs1) * 16 + c;
-      f32x4 acc[2];
-      tile.logits(qlds + (i * 16 + c) * QB::STRIDE, lane, acc);
-      float x[8];
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) x[kb * 4 + e] = acc[kb][e];
-      if (need_mask) {
-        const int t = r < d.R ? r / d.G : -1;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = t >= lim[j] ? x[j] : -INFINITY;
-      }
-      // raw logits: the scale is positive, so the max commutes with it
-      float mx = x[0];
-#pragma unroll
-      for (int j = 1; j < 8; ++j) mx = fmaxf(mx, x[j]);
-      mx = max_xor32(max_xor16(mx));
-      float z = 0.f;
-      if (mx != -INFINITY) {
-        const float ms = -mx * sc;
-#pragma unroll
-        for (int j = 0; j < 8; ++j) z += __builtin_amdgcn_exp2f(fmaf(x[j], sc, ms));
-      }
-      z = sum_xor32(sum_xor16(z));
-      if (g4 == 0) part[i][w][c] = make_float2(mx == -INFINITY ? -INFINITY : mx * sc, z);
+    const int key = kt * KT + tid;
+    const bool any = key < d.S && (key >= d.V_full || keep_row == nullptr || keep_row[key]);
+    if (!block_any(any, reinterpret_cast<uint32_t*>(lds))) {
+      for (int i = 0; i < nch; ++i)
+        if (tid < CH && row0 + i * cstep + tid < d.R) out[row0 + i * cstep + tid] = make_float2(-INFINITY, 0.f);
+      return;
     }
+  }
+
+  Ring ring;
+  ring.init(q, b, g, d, w, lane, row0, cstep);
+  ring.issue(lds, w);
+  Tile tile;
+  tile.init(lane);
+  tile.load_keys(k + (((size_t)b * d.S + min(key0, d.S - 1)) * d.Hkv + g) * Tile::RB,
+                 (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.S - key0)), lane);
+  if (nch > 1) ring.issue(lds + Ring::CB, w);
+  // Only waves whose keys include a dropped visual key, a text key or the end
+  // of the sequence need a per-element mask: kept visual keys are visible to
+  // every text row, text key V_full + t' to the rows of tokens t >= t'.
+  const bool need_mask = !wave_all_visible(keep_row, key0, d.V_full, d.S, lane);
+  uint32_t kept_vis = 0xFFFFFFFFu, txt = 0u;
+  if (need_mask) {
+    kept_vis = lane_key_bits(keep_row, key0, d.V_full, d.S, lane);
+    txt = lane_key_bits(nullptr, key0, d.S, d.S, lane) & ~lane_key_bits(nullptr, key0, d.V_full, d.S, lane);
+  }
+  const float c = d.scale_log2;
+  const float invG = 1.0f / (float)d.G;
+  wait_vmcnt<0>();
+  __syncthreads();
+
+  int pfirst = 0;  // first chunk of the current combine pass
+  auto body = [&](auto bufc, int i) {
+    constexpr int BUF = decltype(bufc)::value;
+    f32x16 s[2];
+    tile.logits(lds + BUF * Ring::CB, lane, s);
+    // this wave's copies of chunk i+1 are done; after the barrier every wave
+    // has read chunk i and chunk i+1 is visible
+    wait_vmcnt<0>();
     __syncthreads();
-    // combine the four waves per row, in wave order
-    for (int v = tid; v < n * 16; v += 256) {
-      const int i = v >> 4, rr = v & 15;
-      const int r = (first + i * d.rs1) * 16 + rr;
+    if (i + 2 < nch) ring.issue(lds + BUF * Ring::CB, w);
+
+    if (need_mask) {
+      const int r = row0 + i * cstep + lq;
+      int t = -1;
       if (r < d.R) {
+        t = (int)((float)r * invG);
+        t -= t * d.G > r;
+        t += (t + 1) * d.G <= r;
+      }
+      // keys <= V_full + t among the lane's keys, a prefix of the bit order
+      const int n1 = keys_upto(d.V_full + t - key0 - 4 * hl);
+      const uint32_t vis = kept_vis | (txt & (n1 >= 32 ? 0xFFFFFFFFu : ((1u << n1) - 1u)));
+#pragma unroll
+      for (int j = 0; j < 32; ++j) s[j >> 4][j & 15] = ((vis >> j) & 1u) ? s[j >> 4][j & 15] : -INFINITY;
+    }
+    // raw logits: the scale is positive, so the max commutes with it
+    float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][r], s[1][r]));
+    mx = max_xor32(mx);
+    // a row that sees none of the wave's keys has mx = -inf and every term 0
+    const float ms = mx == -INFINITY ? 0.f : -mx * c;
+    float z4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z4[r & 3] += __builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms));
+    const float z = sum_xor32((z4[0] + z4[1]) + (z4[2] + z4[3]));
+    if (hl == 0) part[i - pfirst][w][lq] = make_float2(mx == -INFINITY ? -INFINITY : mx * c, z);
+
+    if (i - pfirst == PMAX - 1 || i == nch - 1) {
+      // combine the four waves of chunks pfirst..i, in wave order
+      __syncthreads();
+      const int pc = tid / CH, rr = tid - pc * CH;
+      const int r = row0 + (pfirst + pc) * cstep + rr;
+      if (pc <= i - pfirst && r < d.R) {
         float m = -INFINITY;
 #pragma unroll
-        for (int ww = 0; ww < kScoreWaves; ++ww) m = fmaxf(m, part[i][ww][rr].x);
+        for (int ww = 0; ww < kScoreWaves; ++ww) m = fmaxf(m, part[pc][ww][rr].x);
         float zz = 0.f;
 #pragma unroll
         for (int ww = 0; ww < kScoreWaves; ++ww) {
-          const float2 p = part[i][ww][rr];
-          if (p.x != -INFINITY) zz += p.y * exp2f(p.x - m);
+          const float2 pp = part[pc][ww][rr];
+          if (pp.x != -INFINITY) zz += pp.y * exp2f(pp.x - m);
         }
         out[r] = make_float2(m, zz);
       }
+      __syncthreads();
+      pfirst = i + 1;
     }
-    __syncthreads();
+  };
+  for (int i = 0; i < nch; i += 2) {
+    body(std::integral_constant<int, 0>{}, i);
+    if (i + 1 < nch) body(std::integral_constant<int, 1>{}, i + 1);
   }
 }
 
@@ -390,84 +484,135 @@ score_rowmerge_kernel(int rows_total, int R, int n_kt, const float2* __restrict_
 }
 
 // ---------------------------------------------------------------- sweep 2
-// grid (n_vt, Hkv, B*rs2) over visual key tiles. Each wave owns 32 keys and
-// accumulates exp2(logit - m)/Z over the workgroup's rows per lane, then sums
-// the 16 rows of a lane group by DPP. Output: colpart[b][g][rs][V_full].
+// Flat grid over columns (b, g, visual key tile vt) x rs2 row splits. Each
+// wave owns 64 keys and accumulates exp2(logit - m)/Z over the workgroup's
+// rows per lane, then sums the 32 rows of a lane half by DPP and a permlane
+// swap into colpart[b][g][split][V_full].
 
 template <int DT, int D>
-__global__ void __launch_bounds__(256)
+__global__ void __launch_bounds__(256, 3)
 score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                      const uint8_t* __restrict__ token_keep, const float2* __restrict__ rowstat,
                      float* __restrict__ colpart) {
   using Tile = typename TileOf<DT, D>::T;
-  using E = typename TileOf<DT, D>::E;
-  using QB = QBlock<Tile::ROW_BYTES>;
-  __shared__ __attribute__((aligned(16))) uint8_t qlds[QB::BYTES];
-  __shared__ float2 rs_lds[QB::CHUNKS * 16];
+  using Ring = QRing<Tile>;
+  // one LDS object (see sweep 1)
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES];
 
+  int col, rs;
+  if (!decode_column(d.B * d.Hkv * d.n_vt, d.rs2, col, rs)) return;
+  const int bg = col / d.n_vt, vt = col - bg * d.n_vt;
+  const int b = bg / d.Hkv, g = bg - b * d.Hkv;
   const uint8_t* q = static_cast<const uint8_t*>(qv);
-  const E* k = static_cast<const E*>(kv);
-  const int vt = blockIdx.x, g = blockIdx.y;
-  const int b = blockIdx.z / d.rs2, rs = blockIdx.z - b * d.rs2;
+  const uint8_t* k = static_cast<const uint8_t*>(kv);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int c = lane & 15, g4 = lane >> 4;
+  const int lq = lane & 31, hl = lane >> 5;
   const int key0 = vt * KT + w * KW;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
   float* out = colpart + (((size_t)b * d.Hkv + g) * d.rs2 + rs) * d.V_full;
-  const int nchunks = (d.R + 15) / 16;
+  const int nch = (d.nchunks - rs + d.rs2 - 1) / d.rs2;
+  const int cstep = d.rs2 * CH;
+  const int row0 = rs * CH;
 
-  bool any = false;
-  if (tid < KT) {
-    const int key = vt * KT + tid;
-    any = key < d.V_full && (keep_row == nullptr || keep_row[key]);
-  }
-  if (!__syncthreads_or(any)) {
-    if (tid < KT && vt * KT + tid < d.V_full) out[vt * KT + tid] = 0.f;
-    return;
-  }
+  const int tkey = vt * KT + tid;
+  const bool tkept = tkey < d.V_full && (keep_row == nullptr || keep_row[tkey]);
+  if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds))) {
+    // no kept key in the tile: its column mass is 0
+    if (tkey < d.V_full) out[tkey] = 0.f;
+  } else {
+    const float2* rstat = rowstat + ((size_t)b * d.Hkv + g) * d.R;
+    // (m, 1/Z) of the lane's row of chunk i; rows past R get m = +inf so that
+    // their terms vanish
+    auto row_stat = [&](int i) {
+      const int r = row0 + i * cstep + lq;
+      const float2 v = rstat[min(r, d.R - 1)];
+      return r < d.R ? v : make_float2(INFINITY, 0.f);
+    };
+    float2 st[2];
+    st[0] = row_stat(0);
+    st[1] = make_float2(INFINITY, 0.f);
 
-  Tile tile;
-  tile.load_keys(k + (((size_t)b * d.S + min(key0, d.V_full)) * d.Hkv + g) * D, (size_t)d.Hkv * D,
-                 max(0, min(KW, d.V_full - key0)), lane);
-  const uint32_t vis = kept_visual_mask(keep_row, key0, d.V_full, d.S, lane);
-  const float2* rstat = rowstat + ((size_t)b * d.Hkv + g) * d.R;
-  const float sc = d.scale_log2;
+    Ring ring;
+    ring.init(q, b, g, d, w, lane, row0, cstep);
+    ring.issue(lds, w);
+    Tile tile;
+    tile.init(lane);
+    tile.load_keys(k + (((size_t)b * d.S + min(key0, d.V_full - 1)) * d.Hkv + g) * Tile::RB,
+                   (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.V_full - key0)), lane);
+    if (nch > 1) ring.issue(lds + Ring::CB, w);
+    const float c = d.scale_log2;
 
-  float col[8];
+    f32x16 acc[2];
 #pragma unroll
-  for (int i = 0; i < 8; ++i) col[i] = 0.f;
-  for (int first = rs; first < nchunks; first += d.rs2 * QB::CHUNKS) {
-    const int n = QB::stage(qlds, q, b, g, first, d.rs2, nchunks, d);
-    for (int v = tid; v < n * 16; v += 256) {
-      const int r = (first + (v >> 4) * d.rs2) * 16 + (v & 15);
-      // rows past R get m = +inf so that their terms vanish
-      rs_lds[v] = r < d.R ? rstat[r] : make_float2(INFINITY, 0.f);
-    }
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+    wait_vmcnt<0>();
     __syncthreads();
-    for (int i = 0; i < n; ++i) {
-      const float2 rsv = rs_lds[i * 16 + c];
-      f32x4 acc[2];
-      tile.logits(qlds + (i * 16 + c) * QB::STRIDE, lane, acc);
+
+    auto body = [&](auto bufc, int i) {
+      constexpr int BUF = decltype(bufc)::value;
+      f32x16 s[2];
+      tile.logits(lds + BUF * Ring::CB, lane, s);
+      wait_vmcnt<0>();
+      __syncthreads();
+      // the row statistics load goes first: loads complete in order
+      if (i + 1 < nch) st[BUF ^ 1] = row_stat(i + 1);
+      if (i + 2 < nch) ring.issue(lds + BUF * Ring::CB, w);
+      const float ms = -st[BUF].x, iz = st[BUF].y;
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
+      for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          col[kb * 4 + e] += __builtin_amdgcn_exp2f(fmaf(acc[kb][e], sc, -rsv.x)) * rsv.y;
+        for (int r = 0; r < 16; ++r) acc[nb][r] = fmaf(__builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms)), iz, acc[nb][r]);
+    };
+    for (int i = 0; i < nch; i += 2) {
+      body(std::integral_constant<int, 0>{}, i);
+      if (i + 1 < nch) body(std::integral_constant<int, 1>{}, i + 1);
     }
-    __syncthreads();
+    // sum over the 32 rows of each lane half (lanes sharing lane/32), fixed tree
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[nb][r] = sum_xor16(row16_sum(acc[nb][r]));
+    const uint32_t vis = wave_all_visible(keep_row, key0, d.V_full, d.S, lane)
+                             ? 0xFFFFFFFFu
+                             : lane_key_bits(keep_row, key0, d.V_full, d.S, lane);
+    if (lq == 0) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = key0 + nb * 32 + acc_row(r, hl);
+          // dropped keys were summed over too; their column is forced to 0
+          if (key < d.V_full) out[key] = ((vis >> (nb * 16 + r)) & 1u) ? acc[nb][r] : 0.f;
+        }
+    }
   }
+
+}
+
+// ---------------------------------------------------------------- column sum
+// scores[b][j] = (sum over KV groups g and row splits of colpart[b][g][split][j],
+// in that order) / (Hq*T) for kept visual tokens, -inf for dropped ones.
+
+__global__ void __launch_bounds__(256)
+score_colsum_kernel(int S, int V_full, int nparts, float count, const float* __restrict__ colpart,
+                    const uint8_t* __restrict__ token_keep, float* __restrict__ scores) {
+  const int b = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= V_full) return;
+  const float* cp = colpart + (size_t)b * nparts * V_full + j;
+  float v[8];
+  float sum = 0.f;
+  int p = 0;
+  for (; p + 8 <= nparts; p += 8) {
 #pragma unroll
-  for (int i = 0; i < 8; ++i) col[i] = row16_sum(col[i]);
-  if (c == 0) {
+    for (int u = 0; u < 8; ++u) v[u] = cp[(size_t)(p + u) * V_full];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int key = key0 + kb * 16 + 4 * g4 + e;
-        // dropped keys were summed over too; their column is forced to 0
-        if (key < d.V_full) out[key] = ((vis >> (kb * 4 + e)) & 1u) ? col[kb * 4 + e] : 0.f;
-      }
+    for (int u = 0; u < 8; ++u) sum += v[u];
   }
+  for (; p < nparts; ++p) sum += cp[(size_t)p * V_full];
+  const bool kept = token_keep == nullptr || token_keep[(size_t)b * S + j];
+  scores[(size_t)b * V_full + j] = kept ? sum / count : -INFINITY;
 }
 
 // ---------------------------------------------------------------- top-k + compaction
@@ -488,6 +633,10 @@ __device__ __forceinline__ int keep_count(double r, int V) {
 
 constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
+constexpr int kDigitBits = 12;              // radix digit width of the selection
+constexpr int kBins = 1 << kDigitBits;
+static_assert(kBins == 4 * kTopkThreads, "each thread owns four histogram bins");
+static_assert(LITEVLM_MAX_VISUAL % (4 * kTopkThreads) == 0, "key loads come in whole rounds of float4");
 
 __device__ __forceinline__ int wave_sum_int(int v) {
   float f;  // exact: counts stay far below 2^24
@@ -497,9 +646,34 @@ __device__ __forceinline__ int wave_sum_int(int v) {
   return (int)f;
 }
 
-// Block-wide exclusive scan of one int per thread; returns the exclusive
-// prefix and writes the block total to *total.
-__device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* total) {
+// Nonzero bytes of a 32-bit word.
+__device__ __forceinline__ int nonzero_bytes(uint32_t u) {
+  u |= u >> 4;
+  u |= u >> 2;
+  u |= u >> 1;
+  return __popc(u & 0x01010101u);
+}
+
+// Nonzero flags among row[0..n), counted by one wave (result on every lane).
+__device__ __forceinline__ int wave_count_flags(const uint8_t* row, int n, int lane) {
+  int cnt = 0;
+  if ((reinterpret_cast<uintptr_t>(row) & 15) == 0) {
+    const uint4* r4 = reinterpret_cast<const uint4*>(row);
+    for (int j = lane; j < n / 16; j += 64) {
+      const uint4 u = r4[j];
+      cnt += nonzero_bytes(u.x) + nonzero_bytes(u.y) + nonzero_bytes(u.z) + nonzero_bytes(u.w);
+    }
+    for (int j = (n & ~15) + lane; j < n; j += 64) cnt += row[j] != 0;
+  } else {
+    for (int j = lane; j < n; j += 64) cnt += row[j] != 0;
+  }
+  return wave_sum_int(cnt);
+}
+
+// Block-wide exclusive scan of one int per thread with a single barrier; the
+// 16 wave totals go to wsum, which the caller must not reuse before another
+// barrier. Returns the exclusive prefix; *total gets the block total.
+__device__ __forceinline__ int block_scan_excl(int v, int* wsum, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int x = v;
 #pragma unroll
@@ -509,127 +683,88 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* wsum, int* total
   }
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
-  if (threadIdx.x < 64) {
-    // scan of the 16 wave totals in one wave
-    const int l = threadIdx.x;
-    const int t = l < kTopkWaves ? wsum[l] : 0;
-    int y = t;
+  int before = 0, tot = 0;
 #pragma unroll
-    for (int off = 1; off < kTopkWaves; off <<= 1) {
-      const int u = __shfl_up(y, off, kWave);
-      if (l >= off) y += u;
-    }
-    if (l < kTopkWaves) wsum[kTopkWaves + 1 + l] = y - t;
-    if (l == kTopkWaves - 1) wsum[kTopkWaves] = y;
+  for (int w = 0; w < kTopkWaves; ++w) {
+    const int t = wsum[w];
+    tot += t;
+    before += w < wave ? t : 0;
   }
-  __syncthreads();
-  const int excl = wsum[kTopkWaves + 1 + wave] + x - v;
-  *total = wsum[kTopkWaves];
-  __syncthreads();
-  return excl;
+  *total = tot;
+  return before + x - v;
 }
 
-__device__ __forceinline__ int block_sum(int v, int* wsum) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int s = wave_sum_int(v);
-  if (lane == 0) wsum[wave] = s;
-  __syncthreads();
-  int t = 0;
-#pragma unroll
-  for (int w = 0; w < kTopkWaves; ++w) t += wsum[w];
-  __syncthreads();
-  return t;
-}
-
-// One workgroup per sample: V_b and the compacted offset, scores from the
-// column-mass partials, radix select of the k_b-th largest order key, then
+// One workgroup per sample: the compacted offset from every earlier sample's
+// kept-visual count, order keys of the scores, radix select of the k_b-th
+// largest key (12-bit digits below the common prefix of the kept keys), then
 // the stable compaction.
 __global__ void __launch_bounds__(kTopkThreads)
-topk_compact_kernel(int S, int V_full, int Hkv, int rs2, float count, double keep_ratio,
-                    const float* __restrict__ colpart, const uint8_t* __restrict__ token_keep,
-                    float* __restrict__ scores, int32_t* __restrict__ kept_index,
+topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restrict__ token_keep,
+                    const float* __restrict__ scores, int32_t* __restrict__ kept_index,
                     int32_t* __restrict__ cu_seqlens) {
   __shared__ uint32_t keys[LITEVLM_MAX_VISUAL];
-  __shared__ int hist[kTopkWaves][257];
-  __shared__ int tot[256];
-  __shared__ int wsum[2 * kTopkWaves + 2];
+  __shared__ int hist[kBins];
+  __shared__ int vcnt[LITEVLM_MAX_BATCH];
+  __shared__ int wsum[4][kTopkWaves];  // [0] batch offset, [1], [2] radix passes, [3] compaction
   __shared__ uint32_t red_u[2][kTopkWaves];
   __shared__ int sel_digit, sel_above;
   const int b = blockIdx.x;
   const int T = S - V_full;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-  // Compacted offsets: every sample's length is k_b + T with k_b from its own
-  // kept-visual count, so the prefix is recomputed here from token_keep.
-  int cu_b = 0, V_b = V_full;
-  for (int bb = 0; bb <= b; ++bb) {
-    int Vbb = V_full;
-    if (token_keep) {
-      int cnt = 0;
-      const uint8_t* row = token_keep + (size_t)bb * S;
-      if ((reinterpret_cast<uintptr_t>(row) & 15) == 0) {
-        // 16 flags (0/1 bytes) per load, summed with a byte-wise multiply
-        const uint4* r4 = reinterpret_cast<const uint4*>(row);
-        for (int j = tid; j < V_full / 16; j += kTopkThreads) {
-          const uint4 u = r4[j];
-          cnt += (int)((((u.x & 0x01010101u) * 0x01010101u) >> 24) + (((u.y & 0x01010101u) * 0x01010101u) >> 24) +
-                       (((u.z & 0x01010101u) * 0x01010101u) >> 24) + (((u.w & 0x01010101u) * 0x01010101u) >> 24));
-        }
-        for (int j = (V_full & ~15) + tid; j < V_full; j += kTopkThreads) cnt += row[j] != 0;
-      } else {
-        for (int j = tid; j < V_full; j += kTopkThreads) cnt += row[j] != 0;
-      }
-      Vbb = block_sum(cnt, wsum);
-    }
-    if (bb < b) cu_b += keep_count(keep_ratio, Vbb) + T;
-    else V_b = Vbb;
+  // Kept-visual counts of samples 0..b, one sample per wave at a time.
+  for (int bb = wave; bb <= b; bb += kTopkWaves) {
+    const int c = token_keep ? wave_count_flags(token_keep + (size_t)bb * S, V_full, lane) : V_full;
+    if (lane == 0) vcnt[bb] = c;
   }
-  const int kb_ = keep_count(keep_ratio, V_b);
+  for (int i = tid; i < kBins; i += kTopkThreads) hist[i] = 0;
 
-  // Scores: fixed-order sum over KV groups and row splits, then the mean over
-  // Hq*T rows. Kept keys are >= 0x80000000; dropped tokens get key 0. Each
-  // thread takes 4 consecutive keys so that all partial loads are in flight.
+  // Order keys of the kept tokens' scores (dropped tokens: key 0; kept keys
+  // are >= 0x80000000 since scores are >= 0); loads are unconditional from
+  // clamped addresses so that a thread's rounds are all in flight at once.
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * S : nullptr;
-  const float* cp = colpart + (size_t)b * Hkv * rs2 * V_full;
-  const int nparts = Hkv * rs2;
+  const float* sc = scores + (size_t)b * V_full;
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
-  for (int j4 = tid * 4; j4 < V_full; j4 += kTopkThreads * 4) {
-    float acc[4] = {0.f, 0.f, 0.f, 0.f};
-    const int nk = min(4, V_full - j4);
-    if (nk == 4 && (V_full & 3) == 0) {
-      int i = 0;
-      for (; i + 4 <= nparts; i += 4) {
-        float4 p[4];
+  const bool vec = V_full >= 4 && (V_full & 3) == 0 && (reinterpret_cast<uintptr_t>(sc) & 15) == 0 &&
+                   (keep_row == nullptr || (reinterpret_cast<uintptr_t>(keep_row) & 3) == 0);
+  if (vec) {
+    constexpr int R4 = LITEVLM_MAX_VISUAL / (4 * kTopkThreads);
+    float4 s4[R4];
+    uint32_t f4[R4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) p[u] = *reinterpret_cast<const float4*>(cp + (size_t)(i + u) * V_full + j4);
+    for (int i = 0; i < R4; ++i) {
+      const int j4 = min(4 * (tid + i * kTopkThreads), V_full - 4);
+      s4[i] = *reinterpret_cast<const float4*>(sc + j4);
+      f4[i] = keep_row ? *reinterpret_cast<const uint32_t*>(keep_row + j4) : 0x01010101u;
+    }
+#pragma unroll
+    for (int i = 0; i < R4; ++i) {
+      const int j4 = 4 * (tid + i * kTopkThreads);
+      if (j4 < V_full) {
+        const float sv[4] = {s4[i].x, s4[i].y, s4[i].z, s4[i].w};
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
-          acc[0] += p[u].x; acc[1] += p[u].y; acc[2] += p[u].z; acc[3] += p[u].w;
+          const bool kept = ((f4[i] >> (8 * u)) & 0xFFu) != 0u;
+          const uint32_t key = kept ? order_key(sv[u]) : 0u;
+          if (kept) {
+            kmin = min(kmin, key);
+            kmax = max(kmax, key);
+          }
+          keys[j4 + u] = key;
         }
       }
-      for (; i < nparts; ++i) {
-        const float4 p = *reinterpret_cast<const float4*>(cp + (size_t)i * V_full + j4);
-        acc[0] += p.x; acc[1] += p.y; acc[2] += p.z; acc[3] += p.w;
-      }
-    } else {
-      for (int i = 0; i < nparts; ++i)
-        for (int u = 0; u < nk; ++u) acc[u] += cp[(size_t)i * V_full + j4 + u];
     }
-    for (int u = 0; u < nk; ++u) {
-      const int j = j4 + u;
-      float s = -INFINITY;
-      uint32_t key = 0u;
-      if (keep_row == nullptr || keep_row[j]) {
-        s = acc[u] / count;
-        key = order_key(s);
+  } else {
+    for (int j = tid; j < V_full; j += kTopkThreads) {
+      const bool kept = keep_row == nullptr || keep_row[j];
+      const uint32_t key = kept ? order_key(sc[j]) : 0u;
+      if (kept) {
         kmin = min(kmin, key);
         kmax = max(kmax, key);
       }
-      scores[(size_t)b * V_full + j] = s;
       keys[j] = key;
     }
   }
-  // block min / max of the kept keys
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, off, kWave));
@@ -647,6 +782,18 @@ topk_compact_kernel(int S, int V_full, int Hkv, int rs2, float count, double kee
     kmin = min(kmin, red_u[0][w]);
     kmax = max(kmax, red_u[1][w]);
   }
+  // compacted offset of this sample: sum over earlier samples of k_bb + T
+  int cu_b;
+  {
+    const int term = tid < b ? keep_count(keep_ratio, vcnt[tid]) + T : 0;
+    const int wsm = wave_sum_int(term);
+    if (lane == 0) wsum[0][wave] = wsm;
+    __syncthreads();
+    cu_b = 0;
+#pragma unroll
+    for (int w = 0; w < kTopkWaves; ++w) cu_b += wsum[0][w];
+  }
+  const int kb_ = keep_count(keep_ratio, vcnt[b]);
 
   // Radix select of the kb_-th largest key. Bits above the highest bit where
   // kmin and kmax differ are common to every kept key and are skipped.
@@ -655,77 +802,56 @@ topk_compact_kernel(int S, int V_full, int Hkv, int rs2, float count, double kee
   uint32_t pmask = bits_left == 32 ? 0u : ~((1u << bits_left) - 1u);
   uint32_t prefix = kmax & pmask;
   int krem = kb_;
+  constexpr int KPT = LITEVLM_MAX_VISUAL / kTopkThreads;
+  int pass = 0;
   if (kb_ > 0) {
     while (bits_left > 0) {
-      const int width = bits_left < 8 ? bits_left : 8;
+      const int width = bits_left < kDigitBits ? bits_left : kDigitBits;
       const int shift = bits_left - width;
       const uint32_t dmask = (1u << width) - 1u;
-      for (int i = tid; i < kTopkWaves * 257; i += kTopkThreads) (&hist[0][0])[i] = 0;
-      __syncthreads();
-      for (int j0 = 0; j0 < V_full; j0 += kTopkThreads) {
-        const int j = j0 + tid;
-        const uint32_t kk = j < V_full ? keys[j] : 0u;
-        const bool cand = j < V_full && kk != 0u && (kk & pmask) == prefix;
-        const int digit = (int)((kk >> shift) & dmask);
-        // wave-aggregated count of the most common case: lanes sharing the
-        // first candidate lane's digit add with one atomic
-        const uint64_t active = __ballot(cand);
-        if (active) {
-          const int leader = __ffsll((unsigned long long)active) - 1;
-          const int d0 = __builtin_amdgcn_readlane(digit, leader);
-          const uint64_t same = __ballot(cand && digit == d0);
-          if (lane == leader) atomicAdd(&hist[wave][d0], __popcll(same));
-          if (cand && digit != d0) atomicAdd(&hist[wave][digit], 1);
+#pragma unroll
+      for (int i = 0; i < KPT; ++i) {
+        const int j = tid + i * kTopkThreads;
+        if (j < V_full) {
+          const uint32_t kk = keys[j];
+          if (kk != 0u && (kk & pmask) == prefix) atomicAdd(&hist[(kk >> shift) & dmask], 1);
         }
       }
       __syncthreads();
-      if (tid < 256) {
-        int t = 0;
-#pragma unroll
-        for (int w = 0; w < kTopkWaves; ++w) t += hist[w][tid];
-        tot[tid] = t;
-      }
-      __syncthreads();
-      if (tid < 64) {
-        // lane l owns bins 4l..4l+3; suffix sums over lanes find the bin that
-        // holds the krem-th largest candidate
-        const int l = tid;
-        const int c0 = tot[4 * l], c1 = tot[4 * l + 1], c2 = tot[4 * l + 2], c3 = tot[4 * l + 3];
-        int suf = c0 + c1 + c2 + c3;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-          const int y = __shfl_down(suf, off, kWave);
-          if (l + off < 64) suf += y;
+      // thread t owns bins 4t..4t+3; "above" counts candidates in higher bins
+      const int c0 = hist[4 * tid], c1 = hist[4 * tid + 1], c2 = hist[4 * tid + 2], c3 = hist[4 * tid + 3];
+      const int csum = c0 + c1 + c2 + c3;
+      int total;
+      const int excl = block_scan_excl(csum, wsum[1 + (pass & 1)], &total);
+      const int above = total - excl - csum;
+      // bins are cleared for the next pass by their owners
+      hist[4 * tid] = hist[4 * tid + 1] = hist[4 * tid + 2] = hist[4 * tid + 3] = 0;
+      if (above < krem && above + csum >= krem) {
+        int a = above, dsel;
+        if (a + c3 >= krem) {
+          dsel = 4 * tid + 3;
+        } else if ((a += c3) + c2 >= krem) {
+          dsel = 4 * tid + 2;
+        } else if ((a += c2) + c1 >= krem) {
+          dsel = 4 * tid + 1;
+        } else {
+          a += c1;
+          dsel = 4 * tid;
         }
-        int above = __shfl_down(suf, 1, kWave);  // candidates in bins of lanes > l
-        if (l == 63) above = 0;
-        if (above < krem && suf >= krem) {
-          // walk this lane's bins from the top; a = candidates in higher bins
-          int a = above, dsel;
-          if (a + c3 >= krem) {
-            dsel = 4 * l + 3;
-          } else if ((a += c3) + c2 >= krem) {
-            dsel = 4 * l + 2;
-          } else if ((a += c2) + c1 >= krem) {
-            dsel = 4 * l + 1;
-          } else {
-            a += c1;
-            dsel = 4 * l;
-          }
-          sel_digit = dsel;
-          sel_above = a;
-        }
+        sel_digit = dsel;
+        sel_above = a;
       }
       __syncthreads();
       prefix |= ((uint32_t)sel_digit) << shift;
       pmask |= dmask << shift;
       krem -= sel_above;
       bits_left -= width;
-      __syncthreads();
+      ++pass;
     }
   }
   // prefix is now the kb_-th largest key; take every larger key plus the first
-  // krem equal keys in position order.
+  // krem equal keys in position order. One scan of (larger, equal) counts
+  // packed as 16-bit halves gives both prefixes.
   const uint32_t thr = prefix;
   const int per = (V_full + kTopkThreads - 1) / kTopkThreads;
   const int j0 = min(V_full, tid * per), j1 = min(V_full, j0 + per);
@@ -736,20 +862,20 @@ topk_compact_kernel(int S, int V_full, int Hkv, int rs2, float count, double kee
       neq += kk == thr;
       ngt += kk > thr;
     }
-  int tot_eq;
-  const int eq_before = block_exclusive_scan(neq, wsum, &tot_eq);
-  const int nsel = ngt + max(0, min(neq, krem - eq_before));
-  int tot_sel;
-  const int sel_before = block_exclusive_scan(nsel, wsum, &tot_sel);
+  int tot_packed;
+  const int before = block_scan_excl((ngt << 16) | neq, wsum[3], &tot_packed);
   int32_t* out = kept_index + cu_b;
   if (kb_ > 0) {
-    int eqr = eq_before, pos = sel_before;
+    int gtr = before >> 16, eqr = before & 0xFFFF;
     for (int j = j0; j < j1; ++j) {
       const uint32_t kk = keys[j];
-      bool take = false;
-      if (kk > thr) take = true;
-      else if (kk == thr) { take = eqr < krem; ++eqr; }
-      if (take) out[pos++] = j;
+      if (kk > thr) {
+        out[gtr + min(eqr, krem)] = j;
+        ++gtr;
+      } else if (kk == thr) {
+        if (eqr < krem) out[gtr + eqr] = j;
+        ++eqr;
+      }
     }
   }
   for (int t = tid; t < T; t += kTopkThreads) out[kb_ + t] = V_full + t;
@@ -831,19 +957,19 @@ gather_rows_kernel(int B, int S, const int32_t* __restrict__ kept_index,
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
-  // Row chunks are split over workgroups until a sweep has ~2 workgroups per
-  // CU (256 CUs); sweep 2 splits less since every split multiplies the
-  // column partials top-k must read.
+  // Row chunks are split over workgroups while the sweep fits one pass of the
+  // chip: about four workgroups per CU for sweep 1 and three for sweep 2
+  // (their register budgets), 256 CUs. Sweep 2 splits at most 4 ways since
+  // every split multiplies the column partials top-k must read.
   ScoreSplit p;
   const int T = S - V_full;
   const int R = (Hq / Hkv) * T;
   p.n_kt = (S + KT - 1) / KT;
   p.n_vt = (V_full + KT - 1) / KT;
-  p.nchunks = (R + 15) / 16;
-  const long long w1 = (long long)p.n_kt * Hkv * B, w2 = (long long)p.n_vt * Hkv * B;
-  p.rs1 = (int)std::min<long long>(p.nchunks, std::max<long long>(1, (512 + w1 - 1) / w1));
-  p.rs2 = w2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4),
-                                                std::max<long long>(1, (256 + w2 - 1) / w2));
+  p.nchunks = (R + CH - 1) / CH;
+  const long long c1 = (long long)p.n_kt * Hkv * B, c2 = (long long)p.n_vt * Hkv * B;
+  p.rs1 = (int)std::min<long long>(p.nchunks, std::max<long long>(1, 1024 / c1));
+  p.rs2 = c2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4), std::max<long long>(1, 768 / c2));
   return p;
 }
 
@@ -858,17 +984,23 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv)
   return w;
 }
 
+// Flat XCD-aware grids: 8 XCDs x (columns per XCD, rounded up) x splits.
+static int sweep_grid(long long ncol, int nsplit) { return (int)(8 * ((ncol + 7) / 8) * nsplit); }
+
 template <int DT, int D>
 static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp,
                           float2* rowpart, float2* rowstat, float* colpart, hipStream_t stream) {
-  hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sp.n_kt, a.Hkv, a.B * sp.rs1), dim3(256), 0,
-                     stream, d, a.q, a.k, a.token_keep, rowpart);
+  hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_kt, sp.rs1)),
+                     dim3(256), 0, stream, d, a.q, a.k, a.token_keep, rowpart);
   const int rows_total = a.B * a.Hkv * d.R;
   hipLaunchKernelGGL(score_rowmerge_kernel, dim3((rows_total + 63) / 64), dim3(256), 0, stream,
                      rows_total, d.R, d.n_kt, rowpart, rowstat);
   if (sp.n_vt > 0)
-    hipLaunchKernelGGL((score_colmass_kernel<DT, D>), dim3(sp.n_vt, a.Hkv, a.B * sp.rs2), dim3(256), 0,
-                       stream, d, a.q, a.k, a.token_keep, rowstat, colpart);
+    hipLaunchKernelGGL((score_colmass_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_vt, sp.rs2)),
+                       dim3(256), 0, stream, d, a.q, a.k, a.token_keep, rowstat, colpart);
+  if (sp.n_vt > 0)
+    hipLaunchKernelGGL(score_colsum_kernel, dim3(sp.n_vt, a.B), dim3(256), 0, stream, a.S, a.V_full,
+                       a.Hkv * sp.rs2, (float)a.Hq * (float)d.T, colpart, a.token_keep, a.scores);
 }
 
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
@@ -879,6 +1011,7 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   float2* rowstat = reinterpret_cast<float2*>(ws + w.rowstat_off);
   float* colpart = reinterpret_cast<float*>(ws + w.colpart_off);
   ScoreDims d;
+  d.B = a.B;
   d.S = a.S;
   d.V_full = a.V_full;
   d.T = a.S - a.V_full;
@@ -886,7 +1019,9 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.Hkv = a.Hkv;
   d.G = a.Hq / a.Hkv;
   d.R = d.G * d.T;
+  d.nchunks = sp.nchunks;
   d.n_kt = sp.n_kt;
+  d.n_vt = sp.n_vt;
   d.rs1 = sp.rs1;
   d.rs2 = sp.rs2;
   d.scale_log2 = a.logit_scale_log2;
@@ -900,8 +1035,7 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
 #undef LITEVLM_SWEEPS
 
   hipLaunchKernelGGL(topk_compact_kernel, dim3(a.B), dim3(kTopkThreads), 0, stream, a.S, a.V_full,
-                     a.Hkv, sp.rs2, (float)a.Hq * (float)d.T, a.keep_ratio, colpart, a.token_keep,
-                     a.scores, a.kept_index, a.cu_seqlens);
+                     a.keep_ratio, a.token_keep, a.scores, a.kept_index, a.cu_seqlens);
   if (a.qc || a.kc || a.vc) {
     const int esz = a.dtype == LITEVLM_F32 ? 4 : (a.dtype == LITEVLM_BF16 ? 2 : 1);
     const int qvec = a.Hq * a.D * esz / 16, kvvec = a.Hkv * a.D * esz / 16;

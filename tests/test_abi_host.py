@@ -87,7 +87,7 @@ def test_workspace_size():
     lib = lv.load()
     n = lib.litevlm_token_score_topk_workspace(1, 6272, 6144, 32, 8, 128)
     # per-tile row stats + merged row stats + per-group column mass
-    R, n_kt = 4 * 128, math.ceil(6272 / 128)
+    R, n_kt = 4 * 128, math.ceil(6272 / 256)
     assert n >= 8 * 8 * n_kt * R + 8 * 8 * R + 4 * 8 * 6144
     assert n % 256 == 0
     assert lib.litevlm_token_score_topk_workspace(1, 10, 10, 8, 2, 128) == 0    # no text token
