@@ -202,21 +202,47 @@ attn_bf16_kernel(AttnParams p) {
     const int k0 = t * BN;
     if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);   // buffer last read in step t-1
     if (!(CAUSAL && k0 > wave_q0 + 31)) {
-      // ---- S^T blocks: 2 x (32 keys x 32 queries)
+      // ---- S^T blocks: 2 x (32 keys x 32 queries). K operands are read from
+      // LDS two k-steps ahead of their MFMAs (a ring of three).
       const uint8_t* kl = kvl + buf * TB;
+      const uint8_t* vl = kvl + (2 + buf) * TB;
       f32x16 s[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
         for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+      auto kread = [&](int ks, int nb) __attribute__((always_inline)) {
+        return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[ks]));
+      };
+      bf16x8 ka[3][2];
+#pragma unroll
+      for (int ks = 0; ks < 2 && ks < KS; ++ks)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) ka[ks][nb] = kread(ks, nb);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 2 < KS) {
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-          const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[ks]));
-          s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qreg[ks], s[nb], 0, 0, 0);
+          for (int nb = 0; nb < 2; ++nb) ka[(ks + 2) % 3][nb] = kread(ks + 2, nb);
         }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks % 3][nb], qreg[ks], s[nb], 0, 0, 0);
       }
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 2 < KS) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      }
+      // V operands of the first P.V k-step, read while the softmax runs
+      auto vread = [&](int kk, int db, int hf) __attribute__((always_inline)) {
+        return __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vl + voff[db] + (16 * kk + 4 * hf) * RB));
+      };
+      s16x4 vr[2][DB][2];
+#pragma unroll
+      for (int db = 0; db < DB; ++db)
+#pragma unroll
+        for (int hf = 0; hf < 2; ++hf) vr[0][db][hf] = vread(0, db, hf);
       // ---- mask (edge tiles only), tile max in raw logit units
       const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
       if (need_mask) {
@@ -228,9 +254,9 @@ attn_bf16_kernel(AttnParams p) {
             if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
           }
       }
-      float mx = fmaxf(s[0][0], s[1][0]);
+      float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
 #pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
+      for (int r = 1; r < 16; ++r) mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][r], s[1][r]));
       mx = max_xor32(mx);
       // ---- lazy rescale
       const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
@@ -260,16 +286,25 @@ attn_bf16_kernel(AttnParams p) {
                         (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
       }
       l_run += rs;
-      const uint8_t* vl = kvl + (2 + buf) * TB;
+      // ---- O^T += V^T P^T; V operands one k-step ahead of their MFMAs
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
+        if (kk + 1 < 4) {
+#pragma unroll
+          for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int hf = 0; hf < 2; ++hf) vr[(kk + 1) & 1][db][hf] = vread(kk + 1, db, hf);
+        }
 #pragma unroll
         for (int db = 0; db < DB; ++db) {
-          const s16x4 p0 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vl + voff[db] + (16 * kk) * RB));
-          const s16x4 p1 = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s16x4*)(vl + voff[db] + (16 * kk + 4) * RB));
-          const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(p0, p1, 0, 1, 2, 3, 4, 5, 6, 7));
+          const bf16x8 va = __builtin_bit_cast(bf16x8, __builtin_shufflevector(vr[kk & 1][db][0], vr[kk & 1][db][1], 0, 1, 2, 3, 4, 5, 6, 7));
           o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pb[kk], o[db], 0, 0, 0);
         }
+      }
+#pragma unroll
+      for (int kk = 0; kk < 4; ++kk) {
+        if (kk + 1 < 4) __builtin_amdgcn_sched_group_barrier(0x100, 2 * DB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, DB, 0);
       }
     }
     wait_vmcnt<0>();
@@ -293,7 +328,10 @@ attn_bf16_kernel(AttnParams p) {
 // that a lane half's 32 accumulator values are keys 32*hl .. 32*hl+31, the B
 // operand of one P.V k-step. K rows are 16-byte pieces read directly; V is
 // row-major and read transposed with ds_read_b64_tr_b8 (8 keys per read).
-// P is quantised as p*2^8 under an exact running max.
+// P is quantised as p*2^8 under an exact running max: with the max exact every
+// p is <= 1, and the 2^8 shift keeps p >= 2^-14 out of the E4M3 subnormal
+// range (the lazy rescale of the bf16 path would let p reach 2^TAU, where the
+// coarser E4M3 steps cost accuracy).
 
 typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
