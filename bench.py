@@ -164,19 +164,26 @@ def main():
                 ev[3].record(stream)
 
         def measure(self, r, steps, warmup):
+            """ms per step over `steps` timed steps with no event between the
+            calls (an event record between two kernels adds a gap of a few us to
+            the stream), then the per-call durations from a second pass of the
+            same steps with events around each call."""
             for i in range(warmup):
                 self.step(self.sets[i % len(self.sets)], r)
             torch.cuda.synchronize()
-            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
             t_start = torch.cuda.Event(enable_timing=True)
             t_end = torch.cuda.Event(enable_timing=True)
             torch.cuda.synchronize()
             t_start.record(stream)
             for i in range(steps):
-                self.step(self.sets[i % len(self.sets)], r, evs[i])
+                self.step(self.sets[i % len(self.sets)], r)
             t_end.record(stream)
             torch.cuda.synchronize()
             total_ms = t_start.elapsed_time(t_end)
+            evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(steps)]
+            for i in range(steps):
+                self.step(self.sets[i % len(self.sets)], r, evs[i])
+            torch.cuda.synchronize()
             per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                             for e in evs])
             cu = self.outs["cu_seqlens"].cpu().numpy()

@@ -18,21 +18,12 @@ hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const
                                const float* lexical, float w, float tau, uint8_t* view_keep,
                                uint8_t* token_keep, int32_t* n_visual_kept, hipStream_t stream);
 
-// Keys per workgroup of the two scoring sweeps (4 waves x 64 keys).
-constexpr int kScoreKeyTile = 256;
-
-// Row-chunk split of the two sweeps over workgroups (a function of the shape
-// only, so that the workspace size is too).
-struct ScoreSplit {
-  int n_kt, n_vt, nchunks, rs1, rs2;
-};
-ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv);
-
 // Workspace of the scoring step, carved from one caller buffer:
-//   rowpart  float2 [B][Hkv][n_kt][R]     per-key-tile (max, sum) of each text row
+//   rowpart  float2 [B][Hkv][ns1][R]      per-key-split (max, sum) of each text row
 //   rowstat  float2 [B][Hkv][R]           merged (max, 1/sum) per text row
 //   colpart  float  [B][Hkv][rs2][V_full] column mass per KV group and row split
-// with R = (Hq/Hkv)*T rows per KV group and n_kt = ceil(S / kScoreKeyTile).
+// with R = (Hq/Hkv)*T rows per KV group; ns1 (key splits of sweep 1) and rs2
+// (row splits of sweep 2) are functions of the shape.
 struct ScoreWorkspace {
   size_t rowpart_off, rowstat_off, colpart_off, total;
 };

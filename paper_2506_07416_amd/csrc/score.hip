@@ -7,14 +7,15 @@
 // In original positions that is: kept visual keys (token_keep = 1) and text
 // keys V_full+t' with t' <= t. Exact column mass needs each row's softmax
 // normaliser first, so the work is two sweeps over K:
-//   sweep 1  per (key tile, row): max m and sum Z of exp2(logit) over the tile
-//   merge    per row: m = max over tiles, Z = sum Z_tile * exp2(m_tile - m)
+//   sweep 1  per (key split, row): max m and sum Z of exp2(logit) over the split
+//   merge    per row: m = max over splits, Z = sum Z_split * exp2(m_split - m)
 //   sweep 2  per visual key: sum over rows of exp2(logit - m) / Z
-// Logits are formed transposed, S^T = K Q^T, on 32x32 MFMAs: a wave's 64 keys
-// stay in registers as the A operand and 32 query rows at a time stream
-// through the B operand from LDS. In the 32x32 accumulator a lane owns one
-// query row (lane % 32) and 16 keys per 32-key block. Every reduction runs in
-// a fixed order, so results are deterministic.
+// Both sweeps form logits on 32x32 MFMAs. Sweep 1 keeps 32 query rows per wave
+// in registers and streams key tiles through LDS (a lane owns one query row of
+// the transposed block, so its row statistics stay in the lane). Sweep 2 keeps
+// 64 keys per wave in registers and streams query rows through LDS (a lane owns
+// one key column, so its column mass accumulates in the lane). Every reduction
+// runs in a fixed order, so results are deterministic.
 #include <algorithm>
 #include <type_traits>
 
@@ -23,18 +24,30 @@
 
 namespace litevlm {
 
-constexpr int KW = 64;                    // keys per wave: 2 blocks of 32
-constexpr int kScoreWaves = 4;
-constexpr int KT = KW * kScoreWaves;      // keys per workgroup
-constexpr int CH = 32;                    // text rows per chunk
-constexpr int PMAX = 8;                   // chunks whose row statistics are combined at once
-static_assert(KT == kScoreKeyTile, "workspace layout and kernels disagree on the key tile");
+// sweep 1
+constexpr int KB = 64;                      // keys per key tile
+constexpr int kSweepWaves = 16;             // waves per sweep-1 workgroup, 32 query rows each
+constexpr int kSweepThreads = 64 * kSweepWaves;
+constexpr int RBLK = 32 * kSweepWaves;      // query rows per sweep-1 workgroup
+constexpr int kMaxSplitTiles = 64;          // key tiles per split (one 64-bit live mask)
+// sweep 2
+constexpr int KW = 64;                      // keys per wave: 2 blocks of 32
+constexpr int kColWaves = 4;                // waves per sweep-2 workgroup
+constexpr int KT = KW * kColWaves;          // keys per sweep-2 workgroup
+constexpr int CH = 32;                      // query rows per chunk
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Work split of the sweeps (a function of the shape only, so that the
+// workspace size is too).
+struct ScoreSplit {
+  int n_rb, n_kt, ns1;      // sweep 1: row blocks of RBLK rows, key tiles of KB keys, key splits
+  int n_vt, nchunks, rs2;   // sweep 2: visual key tiles of KT keys, row chunks of CH rows, row splits
+};
+
 struct ScoreDims {
-  int B, S, V_full, T, Hq, Hkv, G, R, nchunks;
-  int n_kt, n_vt, rs1, rs2;
+  int B, S, V_full, T, Hq, Hkv, G, R;
+  int n_rb, n_kt, ns1, n_vt, nchunks, rs2;
   float scale_log2;
 };
 
@@ -45,8 +58,8 @@ __device__ __forceinline__ void wait_vmcnt() {
 
 // Flat, XCD-aware work decode. Workgroup L runs on XCD L % 8; XCD x takes the
 // contiguous column range [x*ncol/8, (x+1)*ncol/8), every column with all of
-// its row splits, so a key tile and its KV group's query rows are read into
-// one XCD's L2. Returns false for the padding workgroups of the grid.
+// its splits, so the query rows of a (sample, KV group) are read into one
+// XCD's L2. Returns false for the padding workgroups of the grid.
 __device__ __forceinline__ bool decode_column(int ncol, int nsplit, int& col, int& split) {
   const int L = blockIdx.x, x = L & 7, j = L >> 3;
   const int c0 = (int)(((long long)x * ncol) >> 3), c1 = (int)(((long long)(x + 1) * ncol) >> 3);
@@ -57,17 +70,461 @@ __device__ __forceinline__ bool decode_column(int ncol, int nsplit, int& col, in
   return true;
 }
 
-// ---------------------------------------------------------------- logit tiles
-// A tile policy holds one wave's 64 keys of one KV head in registers (the A
-// operand of S^T = K Q^T) and forms, for the 32 query rows of a chunk staged
-// in LDS, s[nb][r] = k(32*nb + acc_row(r)) . q(lane % 32) in fp32, with
-// acc_row(r) = 8*(r/4) + 4*(lane/32) + r%4, the 32x32 accumulator layout.
-// ro[] are the lane's byte offsets of its B-operand pieces within a chunk.
+// ---------------------------------------------------------------- sweep-1 logit tiles
+// A sweep-1 workgroup keeps 32 query rows per wave in registers and streams
+// 64-key tiles of K through LDS (row-major, 16-byte pieces XOR-swizzled per
+// row, copied global -> LDS directly). A tile policy forms the transposed
+// 64 x 32 block of a wave on 32x32 MFMAs, s[nb][r] = S^T[key 32*nb +
+// acc_row(r)][row lane % 32] (a lane owns one query row), with acc_row(r) =
+// 8*(r/4) + 4*(lane/32) + r%4, the 32x32 accumulator layout.
 
 __device__ __forceinline__ int acc_row(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
 
+// Query row r (0 <= r < R) of KV group g is query head g*G + r%G of text token r/G.
+// Rows past R are read as row R-1 (their results are never used).
+struct QRows {
+  const uint8_t* base;  // text token 0, query head g*G of this sample
+  int G, Hq, RB, R;
+  __device__ __forceinline__ const uint8_t* row(int r) const {
+    r = min(r, R - 1);
+    const int t = r / G;
+    return base + ((size_t)t * Hq + (r - t * G)) * RB;
+  }
+};
+
 template <int D>
-struct TileBf16 {
+struct RowTileBf16 {
+  static constexpr int RB = D * 2;        // bytes per row
+  static constexpr int NP = RB / 16;      // 16-byte pieces per row
+  static constexpr int KS = D / 16;       // k-steps of v_mfma_f32_32x32x16_bf16
+  static constexpr int TILE = KB * RB;
+  static constexpr int NBUF = 4;          // key-tile buffers: copies run NBUF-1 tiles ahead
+  static_assert(NP == 2 * KS && (NP & (NP - 1)) == 0, "piece index 2*ks + hl must fit the XOR swizzle");
+  bf16x8 q[KS];
+  // LDS offset of the lane's k-step 0 piece within a tile (key lane % 32); the
+  // piece of k-step ks is at kbase ^ (32*ks), since piece 2*ks + hl equals
+  // (2*ks) ^ hl and the swizzle is an XOR below bit 4 of the row offset
+  uint32_t kbase;
+  // each 16-lane group reads 16 rows x 1 piece: conflict-free
+  __device__ __forceinline__ static int swz(int key) { return key & (NP - 1); }
+
+  // k-step ks of lane half hl holds head dims 16*ks + 8*hl .. +7
+  __device__ __forceinline__ void init(const QRows& qr, int row, int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
+    const uint8_t* p = qr.row(row);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      q[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p + (2 * ks + hl) * 16));
+    kbase = lq * RB + (hl ^ swz(lq)) * 16;  // key 32*nb + lq adds 32*nb*RB
+  }
+
+  // s[nb][r] = S^T[key 32*nb + acc_row(r)][row lane % 32]
+  __device__ __forceinline__ void logits(const uint8_t* kl, f32x16 s[2], const QRows&, int, int) const {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+    // re-derived per tile, so that the compiler does not keep all KS offsets live
+    uint32_t kb = kbase;
+    asm volatile("" : "+v"(kb));
+    auto kread = [&](int ks, int nb) __attribute__((always_inline)) {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + (kb ^ (32u * ks))));
+    };
+    bf16x8 ka[2][2];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) ka[0][nb] = kread(0, nb);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) ka[(ks + 1) & 1][nb] = kread(ks + 1, nb);
+      }
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][nb], q[ks], s[nb], 0, 0, 0);
+    }
+  }
+};
+
+template <int D>
+struct RowTileFp8 {
+  // v_mfma_f32_32x32x64_f8f6f4: a lane supplies 32 consecutive E4M3 bytes per k-step
+  static constexpr int RB = D;
+  static constexpr int NP = RB / 16;
+  static constexpr int KS = D / 64;
+  static constexpr int TILE = KB * RB;
+  static constexpr int NBUF = 4;
+  i32x8 q[KS];
+  uint32_t koff[2 * KS];
+  // rows 2i, 2i+1 fill 16 banks-groups between them: conflict-free
+  __device__ __forceinline__ static int swz(int key) { return (key >> 1) & (NP - 1); }
+
+  // k-step ks of lane half hl holds bytes 64*ks + 32*hl .. +31
+  __device__ __forceinline__ void init(const QRows& qr, int row, int lane) {
+    const int lq = lane & 31, hl = lane >> 5;
+    const uint8_t* p = qr.row(row);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int piece = 4 * ks + 2 * hl;
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(p + piece * 16);
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(p + piece * 16 + 16);
+      q[ks] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+#pragma unroll
+      for (int hp = 0; hp < 2; ++hp) koff[2 * ks + hp] = lq * RB + ((piece + hp) ^ swz(lq)) * 16;
+    }
+  }
+
+  // s[nb][r] = S^T[key 32*nb + acc_row(r)][row lane % 32]
+  __device__ __forceinline__ void logits(const uint8_t* kl, f32x16 s[2], const QRows&, int, int) const {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) {
+        const u32x4 lo = *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[2 * ks]);
+        const u32x4 hi = *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[2 * ks + 1]);
+        const i32x8 kb = {(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
+        // format 0 = E4M3 for both operands; zero scale operands select the unscaled instruction
+        s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kb, q[ks], s[nb], 0, 0, 0, 0, 0, 0);
+      }
+    }
+  }
+};
+
+template <int D>
+struct RowTileF32 {
+  // Plain fp32 FMAs; fp32 inputs are only used at small sizes. Query rows are
+  // read from global memory, keys from the LDS tile (unswizzled).
+  static constexpr int RB = D * 4;
+  static constexpr int NP = RB / 16;
+  static constexpr int TILE = KB * RB;
+  static constexpr int NBUF = TILE >= 32768 ? 3 : 4;  // LDS budget of the 32 KB fp32 tiles
+  __device__ __forceinline__ static int swz(int) { return 0; }
+  __device__ __forceinline__ void init(const QRows&, int, int) {}
+
+  // row0: the wave's first query row
+  __device__ __forceinline__ void logits(const uint8_t* kl, f32x16 s[2], const QRows& qr, int row0, int lane) const {
+    const int lq = lane & 31, hl = lane >> 5;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = 32 * nb + acc_row(r, hl);
+        const float* qf = reinterpret_cast<const float*>(qr.row(row0 + lq));
+        const float* kf = reinterpret_cast<const float*>(kl + key * RB);
+        float acc = 0.f;
+        for (int dd = 0; dd < D; ++dd) acc = fmaf(qf[dd], kf[dd], acc);
+        s[nb][r] = acc;
+      }
+  }
+};
+
+template <int DT, int D>
+struct RowTileOf;
+template <int D> struct RowTileOf<LITEVLM_BF16, D> { using T = RowTileBf16<D>; };
+template <int D> struct RowTileOf<LITEVLM_FP8_E4M3, D> { using T = RowTileFp8<D>; };
+template <int D> struct RowTileOf<LITEVLM_F32, D> { using T = RowTileF32<D>; };
+
+// Key tiles of one split, streamed through a ring of NBUF LDS buffers with
+// direct global -> LDS copies (1 KB per wave instruction, keys clamped to
+// klim - 1, pieces swizzled by the tile policy). Every tile of the split is
+// copied, live or not, so that each wave's count of copies in flight is known.
+template <class Tile>
+struct KeyPipe {
+  static constexpr int IPC = Tile::TILE / 1024;  // wave copies per tile
+  static constexpr int NB = Tile::NBUF;
+  static_assert(Tile::TILE % 1024 == 0, "a key tile must split into whole wave copies");
+  uint8_t* ring;
+  const uint8_t* kg;  // key 0 of this sample and KV head
+  size_t kvrow;
+  int tile0, ntl, klim, w, lane, cpw;
+
+  __device__ __forceinline__ KeyPipe(uint8_t* r, const uint8_t* k, size_t kv, int t0, int n, int lim, int w_, int l)
+      : ring(r), kg(k), kvrow(kv), tile0(t0), ntl(n), klim(lim), w(w_), lane(l) {
+    cpw = w < IPC ? (IPC - 1 - w) / kSweepWaves + 1 : 0;  // this wave's copies per tile
+  }
+  __device__ __forceinline__ const uint8_t* buf(int t) const { return ring + (t % NB) * Tile::TILE; }
+  __device__ __forceinline__ void issue(int t) {
+    if (t >= ntl) return;
+    uint8_t* dst = ring + (t % NB) * Tile::TILE;
+    const int key0 = (tile0 + t) * KB;
+    for (int sub = w; sub < IPC; sub += kSweepWaves) {
+      const int slot = sub * 64 + lane;
+      const int row = slot / Tile::NP, ph = slot - row * Tile::NP;
+      const int key = min(key0 + row, klim - 1);
+      __builtin_amdgcn_global_load_lds((const void*)(kg + key * kvrow + (ph ^ Tile::swz(row)) * 16),
+                                       (__attribute__((address_space(3))) void*)(dst + sub * 1024), 16, 0, 0);
+    }
+  }
+  // Wait until this wave's copies of tile t have landed; the copies of the
+  // tiles after it (at most NB-2 of them) may stay in flight. Loads complete
+  // in order, and nothing else is issued between the copies.
+  __device__ __forceinline__ void wait_for(int t) const {
+    const int pend = max(0, min(NB - 2, ntl - 1 - t)) * cpw;
+    switch (pend) {
+      case 0: wait_vmcnt<0>(); break;
+      case 1: wait_vmcnt<1>(); break;
+      case 2: wait_vmcnt<2>(); break;
+      case 3: wait_vmcnt<3>(); break;
+      default: wait_vmcnt<4>(); break;
+    }
+  }
+};
+
+// Live and plain flags of the split's key tiles (bit j for tile tile0 + j):
+// live = some key visible to some row (limit = S: kept visual or text key;
+// limit = V_full: kept visual key), plain = all 64 keys kept visual. The keep
+// bytes (kf, loaded by the caller: f[i] for tile w + 16*i, key lane) are also
+// stored to keepl[tile][key] for the per-element masks.
+constexpr int kFlagsPer = kMaxSplitTiles / kSweepWaves;
+
+__device__ __forceinline__ void load_keep_bytes(const uint8_t* keep_row, int tile0, int V_full, int w, int lane,
+                                                uint8_t f[kFlagsPer]) {
+#pragma unroll
+  for (int i = 0; i < kFlagsPer; ++i) {
+    const int key = (tile0 + w + kSweepWaves * i) * KB + lane;
+    f[i] = (keep_row && V_full > 0) ? keep_row[min(key, V_full - 1)] : 1;
+  }
+}
+
+__device__ __forceinline__ void tile_flags(uint64_t* mw, uint8_t* keepl, const uint8_t f[kFlagsPer], int tile0,
+                                           int ntl, int V_full, int limit, int w, int lane, uint64_t& live,
+                                           uint64_t& plain) {
+  // each wave writes the bits of its own tiles into its own words; no atomics
+  uint64_t lv_w = 0, pl_w = 0;
+#pragma unroll
+  for (int i = 0; i < kFlagsPer; ++i) {
+    const int j = w + kSweepWaves * i;
+    const int key = (tile0 + j) * KB + lane;
+    const bool vis = key < V_full && f[i] != 0;
+    const bool txt = key >= V_full && key < limit;
+    const uint64_t lv = __ballot(vis || txt), pl = __ballot(vis);
+    if (j < ntl) {
+      keepl[j * KB + lane] = vis ? 1 : 0;
+      lv_w |= (lv != 0ull ? 1ull : 0ull) << j;
+      pl_w |= (pl == ~0ull ? 1ull : 0ull) << j;
+    }
+  }
+  if (lane == 0) {
+    mw[w] = lv_w;
+    mw[kSweepWaves + w] = pl_w;
+  }
+  __syncthreads();
+  live = 0;
+  plain = 0;
+#pragma unroll
+  for (int ww = 0; ww < kSweepWaves; ++ww) {
+    live |= mw[ww];
+    plain |= mw[kSweepWaves + ww];
+  }
+}
+
+// Bit j (j = 16*nb + r) of the lane's 32 accumulator keys 32*nb + acc_row(r,
+// lane/32) of tile j0 set where the key is a kept visual key (from the LDS keep
+// bytes, 4 consecutive keys per word). Keys ascend with j.
+__device__ __forceinline__ uint32_t lane_kept_bits(const uint8_t* keepl_tile, int lane) {
+  const int hl = lane >> 5;
+  uint32_t m = 0;
+#pragma unroll
+  for (int q4 = 0; q4 < 8; ++q4) {
+    const uint32_t wd = *reinterpret_cast<const uint32_t*>(keepl_tile + 8 * q4 + 4 * hl);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) m |= ((wd >> (8 * e)) & 1u) << (4 * q4 + e);
+  }
+  return m;
+}
+
+// Number of the lane's 32 accumulator keys that are <= key0 + 4*(lane/32) + L;
+// they form a prefix of the bit order above.
+__device__ __forceinline__ int keys_upto(int L) {
+  int n = 0;
+#pragma unroll
+  for (int q4 = 0; q4 < 8; ++q4) n += min(max(L - 8 * q4 + 1, 0), 4);  // quad q4 holds offsets 8*q4 + 0..3
+  return n;
+}
+
+// ---------------------------------------------------------------- sweep 1
+// Flat grid over (b, g, row block rb) x ns1 key splits. Wave w owns query
+// rows rb*512 + 32w .. +31 (one per lane, S^T layout) and keeps an exact
+// running (max, sum) of exp2(logit) over the split's visible keys; the key
+// tiles stream through a ring of LDS buffers, dead tiles (dropped views only) are
+// not computed. Output: rowpart[b][g][split][row] = (max, sum), max in log2
+// units.
+
+template <int DT, int D>
+__global__ void __launch_bounds__(kSweepThreads)
+score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
+                      const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
+  using Tile = typename RowTileOf<DT, D>::T;
+  // One LDS object (key ring, keep bytes, flag words): with a single object
+  // the compiler adds no vmcnt wait of its own before reads of one buffer
+  // while direct copies into another are in flight; the explicit waits and
+  // barriers order copies before reads.
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tile::NBUF * Tile::TILE + kMaxSplitTiles * KB + 2 * kSweepWaves * 8];
+  uint8_t* keepl = lds + Tile::NBUF * Tile::TILE;
+  uint64_t* mw = reinterpret_cast<uint64_t*>(keepl + kMaxSplitTiles * KB);
+
+  int col, split;
+  if (!decode_column(d.B * d.Hkv * d.n_rb, d.ns1, col, split)) return;
+  const int bg = col / d.n_rb, rb = col - bg * d.n_rb;
+  const int b = bg / d.Hkv, g = bg - b * d.Hkv;
+  const int tile0 = (int)((long long)split * d.n_kt / d.ns1);
+  const int ntl = (int)((long long)(split + 1) * d.n_kt / d.ns1) - tile0;
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int lq = lane & 31, hl = lane >> 5;
+  const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
+  const uint8_t* q = static_cast<const uint8_t*>(qv);
+  const uint8_t* k = static_cast<const uint8_t*>(kv);
+  const QRows qr{q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * Tile::RB, d.G, d.Hq, Tile::RB, d.R};
+  const int row0 = rb * RBLK + 32 * w;
+  const int row = row0 + lq;
+  const bool wave_active = row0 < d.R;
+
+  // keep bytes, the wave's query rows and the first NBUF-1 key tiles, all in flight together
+  uint8_t kf[kFlagsPer];
+  load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
+  Tile tile;
+  if (wave_active) tile.init(qr, row, lane);
+  KeyPipe<Tile> pipe(lds, k + ((size_t)b * d.S * d.Hkv + g) * Tile::RB, (size_t)d.Hkv * Tile::RB, tile0, ntl,
+                     d.S, w, lane);
+#pragma unroll
+  for (int t = 0; t < Tile::NBUF - 1; ++t) pipe.issue(t);
+  pipe.wait_for(0);
+  __syncthreads();  // tile 0 and the keep bytes have landed
+  uint64_t live, plain;
+  tile_flags(mw, keepl, kf, tile0, ntl, d.V_full, d.S, w, lane, live, plain);
+
+  // token of the lane's row for the causal text mask (-1: a row past R sees no text)
+  const int t_row = row < d.R ? row / d.G : -1;
+  const float c = d.scale_log2;
+  float m_run = -INFINITY, z_run = 0.f;
+
+  // Statistics of one tile held in s (masking as needed).
+  auto stats = [&](int t, f32x16* s) __attribute__((always_inline)) {
+    if (!((plain >> t) & 1ull)) {
+      // visible: kept visual keys, and text keys V_full + t' with t' <= the row's token
+      const int key0 = (tile0 + t) * KB;
+      const uint32_t kept = lane_kept_bits(keepl + t * KB, lane);
+      const int nv = keys_upto(d.V_full - 1 - key0 - 4 * hl);   // keys < V_full
+      const int ns = keys_upto(d.S - 1 - key0 - 4 * hl);        // keys < S
+      const int n1 = min(keys_upto(d.V_full + t_row - key0 - 4 * hl), ns);
+      const uint32_t below_n1 = n1 >= 32 ? 0xFFFFFFFFu : ((1u << n1) - 1u);
+      const uint32_t below_nv = nv >= 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+      const uint32_t vis = kept | (below_n1 & ~below_nv);
+#pragma unroll
+      for (int j = 0; j < 32; ++j) s[j >> 4][j & 15] = ((vis >> j) & 1u) ? s[j >> 4][j & 15] : -INFINITY;
+    }
+    // raw logits: the scale is positive, so the max commutes with it
+    float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][r], s[1][r]));
+    mx = max_xor32(mx);
+    const float m_new = fmaxf(m_run, mx);
+    // exact running max: the sum so far is rescaled whenever the max grows
+    const float ms = m_new == -INFINITY ? 0.f : -m_new * c;
+    const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f(fmaf(m_run, c, ms));
+    float z4[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) z4[r & 3] += __builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms));
+    z_run = fmaf(z_run, alpha, (z4[0] + z4[1]) + (z4[2] + z4[3]));
+    m_run = m_new;
+  };
+
+  // Waves w and w+4 share a SIMD. Group 0 (w & 4 == 0) forms the logits of
+  // tile t and then its statistics within step t; group 1 first finishes the
+  // statistics of tile t-1 and then forms the logits of tile t, keeping them
+  // across the barrier. On each SIMD one group's VALU work overlaps the other
+  // group's MFMAs.
+  const bool lag = (w & 4) != 0;
+  f32x16 s[2];
+  for (int t = 0; t < ntl; ++t) {
+    // the buffer of tile t+NBUF-1 was last read in step t-1
+    pipe.issue(t + Tile::NBUF - 1);
+    if (wave_active) {
+      if (lag) {
+        if (t > 0 && ((live >> (t - 1)) & 1ull)) stats(t - 1, s);
+        if ((live >> t) & 1ull) tile.logits(pipe.buf(t), s, qr, row0, lane);
+      } else if ((live >> t) & 1ull) {
+        tile.logits(pipe.buf(t), s, qr, row0, lane);
+        stats(t, s);
+      }
+    }
+    pipe.wait_for(t + 1);
+    __syncthreads();
+  }
+  if (wave_active && lag && ((live >> (ntl - 1)) & 1ull)) stats(ntl - 1, s);
+  // both lane halves share the running max; their sums cover different keys
+  const float z = sum_xor32(z_run);
+  if (hl == 0 && row < d.R)
+    rowpart[(((size_t)b * d.Hkv + g) * d.ns1 + split) * d.R + row] =
+        make_float2(m_run == -INFINITY ? -INFINITY : m_run * c, z);
+}
+
+// ---------------------------------------------------------------- merge
+// One row per (thread % 64); the key splits go to 4 thread slices (split s to
+// slice s % 4), and the slices are combined in slice order. With at most
+// 4*kMergeMax splits a slice holds its values in registers (one pass over
+// memory), otherwise it reads them twice. rowstat = (max in log2 units, 1/sum).
+
+constexpr int kMergeMax = 16;
+
+template <bool REG>
+__global__ void __launch_bounds__(256)
+score_rowmerge_kernel(int rows_total, int R, int nsplit, const float2* __restrict__ rowpart,
+                      float2* __restrict__ rowstat) {
+  __shared__ float red[2][4][64];
+  const int tid = threadIdx.x, slot = tid & 63, slice = tid >> 6;
+  const int idx = blockIdx.x * 64 + slot;
+  const bool ok = idx < rows_total;
+  const int bg = ok ? idx / R : 0, r = ok ? idx - bg * R : 0;
+  const float2* p = rowpart + (size_t)bg * nsplit * R + r;
+  const int mine = ok ? (nsplit - slice + 3) / 4 : 0;  // splits slice, slice + 4, ...
+  float2 v[REG ? kMergeMax : 1];
+  float m = -INFINITY;
+  if (REG) {
+#pragma unroll
+    for (int i = 0; i < kMergeMax; ++i)
+      v[i] = i < mine ? p[(size_t)(slice + 4 * i) * R] : make_float2(-INFINITY, 0.f);
+#pragma unroll
+    for (int i = 0; i < kMergeMax; ++i) m = fmaxf(m, v[i].x);
+  } else {
+    for (int i = 0; i < mine; ++i) m = fmaxf(m, p[(size_t)(slice + 4 * i) * R].x);
+  }
+  red[0][slice][slot] = m;
+  __syncthreads();
+  m = fmaxf(fmaxf(red[0][0][slot], red[0][1][slot]), fmaxf(red[0][2][slot], red[0][3][slot]));
+  float z = 0.f;
+  if (REG) {
+#pragma unroll
+    for (int i = 0; i < kMergeMax; ++i)
+      if (v[i].x != -INFINITY) z += v[i].y * exp2f(v[i].x - m);
+  } else {
+    for (int i = 0; i < mine; ++i) {
+      const float2 u = p[(size_t)(slice + 4 * i) * R];
+      if (u.x != -INFINITY) z += u.y * exp2f(u.x - m);
+    }
+  }
+  red[1][slice][slot] = z;
+  __syncthreads();
+  if (slice == 0 && ok) {
+    const float zt = ((red[1][0][slot] + red[1][1][slot]) + red[1][2][slot]) + red[1][3][slot];
+    rowstat[idx] = make_float2(m, 1.0f / zt);
+  }
+}
+
+// ---------------------------------------------------------------- sweep-2 logit tiles
+// A sweep-2 tile policy holds one wave's 64 keys of one KV head in registers
+// (the A operand of S^T = K Q^T) and forms, for the 32 query rows of a chunk
+// staged in LDS, s[nb][r] = k(32*nb + acc_row(r)) . q(lane % 32) in fp32.
+// ro[] are the lane's byte offsets of its B-operand pieces within a chunk.
+
+template <int D>
+struct ColTileBf16 {
   static constexpr int RB = D * 2;        // bytes per row
   static constexpr int NP = RB / 16;      // 16-byte pieces per row
   static constexpr int KS = D / 16;       // k-steps of v_mfma_f32_32x32x16_bf16
@@ -110,7 +567,7 @@ struct TileBf16 {
 };
 
 template <int D>
-struct TileFp8 {
+struct ColTileFp8 {
   // v_mfma_f32_32x32x64_f8f6f4: a lane supplies 32 consecutive E4M3 bytes per k-step
   static constexpr int RB = D;
   static constexpr int NP = RB / 16;
@@ -161,7 +618,7 @@ struct TileFp8 {
 };
 
 template <int D>
-struct TileF32 {
+struct ColTileF32 {
   // Plain fp32 FMAs; fp32 inputs are only used at small sizes. The lane's 32
   // accumulator keys are read from global memory, its query row from LDS.
   static constexpr int RB = D * 4;
@@ -196,10 +653,10 @@ struct TileF32 {
 };
 
 template <int DT, int D>
-struct TileOf;
-template <int D> struct TileOf<LITEVLM_BF16, D> { using T = TileBf16<D>; };
-template <int D> struct TileOf<LITEVLM_FP8_E4M3, D> { using T = TileFp8<D>; };
-template <int D> struct TileOf<LITEVLM_F32, D> { using T = TileF32<D>; };
+struct ColTileOf;
+template <int D> struct ColTileOf<LITEVLM_BF16, D> { using T = ColTileBf16<D>; };
+template <int D> struct ColTileOf<LITEVLM_FP8_E4M3, D> { using T = ColTileFp8<D>; };
+template <int D> struct ColTileOf<LITEVLM_F32, D> { using T = ColTileF32<D>; };
 
 // Text query rows of a workgroup pass through two chunk buffers in LDS,
 // filled with direct global -> LDS copies (16-byte pieces, XOR-swizzled per
@@ -213,10 +670,10 @@ struct QRing {
   static constexpr int NP = Tile::NP;
   static constexpr int CB = CH * RB;                            // bytes per chunk
   static constexpr int IPC = CB / 1024;                         // wave copies per chunk
-  static constexpr int CPW = (IPC + kScoreWaves - 1) / kScoreWaves;
+  static constexpr int CPW = (IPC + kColWaves - 1) / kColWaves;
   static constexpr int BYTES = 2 * CB;
   static_assert(CB % 1024 == 0, "a chunk must split into whole wave copies");
-  static_assert(IPC % kScoreWaves == 0 || IPC < kScoreWaves, "copies must split evenly over waves");
+  static_assert(IPC % kColWaves == 0 || IPC < kColWaves, "copies must split evenly over waves");
 
   const uint8_t* qbase;  // row (text token 0, head g*G) of this sample and group
   int G, Hq, T, dt, dh;
@@ -233,7 +690,7 @@ struct QRing {
     dh = cstep - dt * d.G;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
-      const int slot = (w + kScoreWaves * j) * 64 + lane;
+      const int slot = (w + kColWaves * j) * 64 + lane;
       const int row = slot / NP;
       src[j] = ((slot % NP) ^ Tile::qswz(row)) * 16;
       const int r = row0 + row;
@@ -246,7 +703,7 @@ struct QRing {
   __device__ __forceinline__ void issue(uint8_t* buf, int w) {
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
-      const int sub = w + kScoreWaves * j;
+      const int sub = w + kColWaves * j;
       if (sub < IPC) {
         const int tt = min(t[j], T - 1);
         __builtin_amdgcn_global_load_lds((const void*)(qbase + ((size_t)tt * Hq + hh[j]) * RB + src[j]),
@@ -301,190 +758,8 @@ __device__ __forceinline__ uint32_t lane_key_bits(const uint8_t* keep_row, int k
   return m;
 }
 
-// Number of the lane's 32 accumulator keys that are <= key0 + 4*(lane/32) + L;
-// they form a prefix of the bit order above.
-__device__ __forceinline__ int keys_upto(int L) {
-  int n = 0;
-#pragma unroll
-  for (int q4 = 0; q4 < 8; ++q4) n += min(max(L - 8 * q4 + 1, 0), 4);  // quad q4 holds offsets 8*q4 + 0..3
-  return n;
-}
-
-// ---------------------------------------------------------------- sweep 1
-// Flat grid over columns (b, g, key tile kt) x rs1 row splits. Wave w holds
-// keys [kt*256 + 64w, +64); the workgroup runs over its row chunks (chunk =
-// split, split + rs1, ...). Per chunk each wave forms its 64 x 32 logits and
-// the per-row (max, sum) over its keys; every PMAX chunks the four waves'
-// statistics are combined in wave order and written to rowpart.
-
-template <int DT, int D>
-__global__ void __launch_bounds__(256, 4)
-score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
-                      const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
-  using Tile = typename TileOf<DT, D>::T;
-  using Ring = QRing<Tile>;
-  // One LDS object (the Q ring, then the per-wave row statistics): with a
-  // single object the compiler adds no vmcnt wait of its own before reads of
-  // one ring buffer while direct copies into the other are in flight; the
-  // explicit wait + barrier at each chunk orders copies before reads.
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES + PMAX * kScoreWaves * CH * sizeof(float2)];
-  float2 (*part)[kScoreWaves][CH] = reinterpret_cast<float2 (*)[kScoreWaves][CH]>(lds + Ring::BYTES);
-
-  int col, rs;
-  if (!decode_column(d.B * d.Hkv * d.n_kt, d.rs1, col, rs)) return;
-  const int bg = col / d.n_kt, kt = col - bg * d.n_kt;
-  const int b = bg / d.Hkv, g = bg - b * d.Hkv;
-  const uint8_t* q = static_cast<const uint8_t*>(qv);
-  const uint8_t* k = static_cast<const uint8_t*>(kv);
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int lq = lane & 31, hl = lane >> 5;
-  const int key0 = kt * KT + w * KW;
-  const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
-  const int nch = (d.nchunks - rs + d.rs1 - 1) / d.rs1;  // chunks rs, rs + rs1, ...
-  const int cstep = d.rs1 * CH;                          // rows between them
-  const int row0 = rs * CH;
-  float2* out = rowpart + (((size_t)b * d.Hkv + g) * d.n_kt + kt) * d.R;
-
-  // A tile of dropped-view keys only (no text key) contributes (-inf, 0).
-  {
-    const int key = kt * KT + tid;
-    const bool any = key < d.S && (key >= d.V_full || keep_row == nullptr || keep_row[key]);
-    if (!block_any(any, reinterpret_cast<uint32_t*>(lds))) {
-      for (int i = 0; i < nch; ++i)
-        if (tid < CH && row0 + i * cstep + tid < d.R) out[row0 + i * cstep + tid] = make_float2(-INFINITY, 0.f);
-      return;
-    }
-  }
-
-  Ring ring;
-  ring.init(q, b, g, d, w, lane, row0, cstep);
-  ring.issue(lds, w);
-  Tile tile;
-  tile.init(lane);
-  tile.load_keys(k + (((size_t)b * d.S + min(key0, d.S - 1)) * d.Hkv + g) * Tile::RB,
-                 (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.S - key0)), lane);
-  if (nch > 1) ring.issue(lds + Ring::CB, w);
-  // Only waves whose keys include a dropped visual key, a text key or the end
-  // of the sequence need a per-element mask: kept visual keys are visible to
-  // every text row, text key V_full + t' to the rows of tokens t >= t'.
-  const bool need_mask = !wave_all_visible(keep_row, key0, d.V_full, d.S, lane);
-  uint32_t kept_vis = 0xFFFFFFFFu, txt = 0u;
-  if (need_mask) {
-    kept_vis = lane_key_bits(keep_row, key0, d.V_full, d.S, lane);
-    txt = lane_key_bits(nullptr, key0, d.S, d.S, lane) & ~lane_key_bits(nullptr, key0, d.V_full, d.S, lane);
-  }
-  const float c = d.scale_log2;
-  const float invG = 1.0f / (float)d.G;
-  wait_vmcnt<0>();
-  __syncthreads();
-
-  int pfirst = 0;  // first chunk of the current combine pass
-  auto body = [&](auto bufc, int i) {
-    constexpr int BUF = decltype(bufc)::value;
-    f32x16 s[2];
-    tile.logits(lds + BUF * Ring::CB, lane, s);
-    // this wave's copies of chunk i+1 are done; after the barrier every wave
-    // has read chunk i and chunk i+1 is visible
-    wait_vmcnt<0>();
-    __syncthreads();
-    if (i + 2 < nch) ring.issue(lds + BUF * Ring::CB, w);
-
-    if (need_mask) {
-      const int r = row0 + i * cstep + lq;
-      int t = -1;
-      if (r < d.R) {
-        t = (int)((float)r * invG);
-        t -= t * d.G > r;
-        t += (t + 1) * d.G <= r;
-      }
-      // keys <= V_full + t among the lane's keys, a prefix of the bit order
-      const int n1 = keys_upto(d.V_full + t - key0 - 4 * hl);
-      const uint32_t vis = kept_vis | (txt & (n1 >= 32 ? 0xFFFFFFFFu : ((1u << n1) - 1u)));
-#pragma unroll
-      for (int j = 0; j < 32; ++j) s[j >> 4][j & 15] = ((vis >> j) & 1u) ? s[j >> 4][j & 15] : -INFINITY;
-    }
-    // raw logits: the scale is positive, so the max commutes with it
-    float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
-#pragma unroll
-    for (int r = 1; r < 16; ++r) mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][r], s[1][r]));
-    mx = max_xor32(mx);
-    // a row that sees none of the wave's keys has mx = -inf and every term 0
-    const float ms = mx == -INFINITY ? 0.f : -mx * c;
-    float z4[4] = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) z4[r & 3] += __builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms));
-    const float z = sum_xor32((z4[0] + z4[1]) + (z4[2] + z4[3]));
-    if (hl == 0) part[i - pfirst][w][lq] = make_float2(mx == -INFINITY ? -INFINITY : mx * c, z);
-
-    if (i - pfirst == PMAX - 1 || i == nch - 1) {
-      // combine the four waves of chunks pfirst..i, in wave order
-      __syncthreads();
-      const int pc = tid / CH, rr = tid - pc * CH;
-      const int r = row0 + (pfirst + pc) * cstep + rr;
-      if (pc <= i - pfirst && r < d.R) {
-        float m = -INFINITY;
-#pragma unroll
-        for (int ww = 0; ww < kScoreWaves; ++ww) m = fmaxf(m, part[pc][ww][rr].x);
-        float zz = 0.f;
-#pragma unroll
-        for (int ww = 0; ww < kScoreWaves; ++ww) {
-          const float2 pp = part[pc][ww][rr];
-          if (pp.x != -INFINITY) zz += pp.y * exp2f(pp.x - m);
-        }
-        out[r] = make_float2(m, zz);
-      }
-      __syncthreads();
-      pfirst = i + 1;
-    }
-  };
-  for (int i = 0; i < nch; i += 2) {
-    body(std::integral_constant<int, 0>{}, i);
-    if (i + 1 < nch) body(std::integral_constant<int, 1>{}, i + 1);
-  }
-}
-
-// ---------------------------------------------------------------- merge
-// One row per (thread % 64), the key tiles split over 4 thread slices and
-// combined in slice order.
-
-__global__ void __launch_bounds__(256)
-score_rowmerge_kernel(int rows_total, int R, int n_kt, const float2* __restrict__ rowpart,
-                      float2* __restrict__ rowstat) {
-  __shared__ float red[4][64];
-  const int tid = threadIdx.x, slot = tid & 63, slice = tid >> 6;
-  const int idx = blockIdx.x * 64 + slot;
-  const bool ok = idx < rows_total;
-  const int bg = ok ? idx / R : 0, r = ok ? idx - bg * R : 0;
-  const float2* p = rowpart + (size_t)bg * n_kt * R + r;
-  float m = -INFINITY;
-  if (ok) {
-#pragma unroll 4
-    for (int kt = slice; kt < n_kt; kt += 4) m = fmaxf(m, p[(size_t)kt * R].x);
-  }
-  red[slice][slot] = m;
-  __syncthreads();
-  m = fmaxf(fmaxf(red[0][slot], red[1][slot]), fmaxf(red[2][slot], red[3][slot]));
-  __syncthreads();
-  float z = 0.f;
-  if (ok) {
-#pragma unroll 4
-    for (int kt = slice; kt < n_kt; kt += 4) {
-      const float2 v = p[(size_t)kt * R];
-      if (v.x != -INFINITY) z += v.y * exp2f(v.x - m);
-    }
-  }
-  red[slice][slot] = z;
-  __syncthreads();
-  if (slice == 0 && ok) {
-    const float zt = ((red[0][slot] + red[1][slot]) + red[2][slot]) + red[3][slot];
-    rowstat[idx] = make_float2(m, 1.0f / zt);
-  }
-}
-
 // ---------------------------------------------------------------- sweep 2
-// Flat grid over columns (b, g, visual key tile vt) x rs2 row splits. Each
+// Flat grid over columns (b, g, visual key tile vt of KT keys) x rs2 row splits. Each
 // wave owns 64 keys and accumulates exp2(logit - m)/Z over the workgroup's
 // rows per lane, then sums the 32 rows of a lane half by DPP and a permlane
 // swap into colpart[b][g][split][V_full].
@@ -494,9 +769,9 @@ __global__ void __launch_bounds__(256, 3)
 score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                      const uint8_t* __restrict__ token_keep, const float2* __restrict__ rowstat,
                      float* __restrict__ colpart) {
-  using Tile = typename TileOf<DT, D>::T;
+  using Tile = typename ColTileOf<DT, D>::T;
   using Ring = QRing<Tile>;
-  // one LDS object (see sweep 1)
+  // one LDS object (see sweep 1): the two query-row chunk buffers
   __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES];
 
   int col, rs;
@@ -614,6 +889,7 @@ score_colsum_kernel(int S, int V_full, int nparts, float count, const float* __r
   const bool kept = token_keep == nullptr || token_keep[(size_t)b * S + j];
   scores[(size_t)b * V_full + j] = kept ? sum / count : -INFINITY;
 }
+
 
 // ---------------------------------------------------------------- top-k + compaction
 
@@ -952,23 +1228,29 @@ gather_rows_kernel(int B, int S, const int32_t* __restrict__ kept_index,
   }
 }
 
+
 // ---------------------------------------------------------------- host launch
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
-  // Row chunks are split over workgroups while the sweep fits one pass of the
-  // chip: about four workgroups per CU for sweep 1 and three for sweep 2
-  // (their register budgets), 256 CUs. Sweep 2 splits at most 4 ways since
-  // every split multiplies the column partials top-k must read.
+static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
+  // Sweep 1: one 16-wave workgroup per CU (256 CUs); the key tiles of each
+  // (sample, KV group, row block) are split until the grid has ~256
+  // workgroups, at most kMaxSplitTiles tiles to one split. Sweep 2: row chunks
+  // are split over workgroups while the grid fits one pass of the chip at
+  // three 4-wave workgroups per CU, at most 4 ways since every split
+  // multiplies the column partials the column sum reads.
   ScoreSplit p;
   const int T = S - V_full;
   const int R = (Hq / Hkv) * T;
-  p.n_kt = (S + KT - 1) / KT;
+  p.n_rb = (R + RBLK - 1) / RBLK;
+  p.n_kt = (S + KB - 1) / KB;
+  const long long cols = std::max<long long>(1, (long long)B * Hkv * p.n_rb);
+  const int want = (int)std::max<long long>(1, 256 / cols);
+  p.ns1 = std::max((p.n_kt + kMaxSplitTiles - 1) / kMaxSplitTiles, std::min(p.n_kt, want));
   p.n_vt = (V_full + KT - 1) / KT;
   p.nchunks = (R + CH - 1) / CH;
-  const long long c1 = (long long)p.n_kt * Hkv * B, c2 = (long long)p.n_vt * Hkv * B;
-  p.rs1 = (int)std::min<long long>(p.nchunks, std::max<long long>(1, 1024 / c1));
+  const long long c2 = (long long)p.n_vt * Hkv * B;
   p.rs2 = c2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4), std::max<long long>(1, 768 / c2));
   return p;
 }
@@ -978,7 +1260,7 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv)
   const size_t R = (size_t)(Hq / Hkv) * (S - V_full);
   ScoreWorkspace w;
   w.rowpart_off = 0;
-  w.rowstat_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.n_kt * R);
+  w.rowstat_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1 * R);
   w.colpart_off = align256(w.rowstat_off + sizeof(float2) * B * Hkv * R);
   w.total = align256(w.colpart_off + sizeof(float) * B * Hkv * (size_t)sp.rs2 * V_full);
   return w;
@@ -990,17 +1272,17 @@ static int sweep_grid(long long ncol, int nsplit) { return (int)(8 * ((ncol + 7)
 template <int DT, int D>
 static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp,
                           float2* rowpart, float2* rowstat, float* colpart, hipStream_t stream) {
-  hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_kt, sp.rs1)),
-                     dim3(256), 0, stream, d, a.q, a.k, a.token_keep, rowpart);
+  hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_rb, sp.ns1)),
+                     dim3(kSweepThreads), 0, stream, d, a.q, a.k, a.token_keep, rowpart);
   const int rows_total = a.B * a.Hkv * d.R;
-  hipLaunchKernelGGL(score_rowmerge_kernel, dim3((rows_total + 63) / 64), dim3(256), 0, stream,
-                     rows_total, d.R, d.n_kt, rowpart, rowstat);
-  if (sp.n_vt > 0)
+  hipLaunchKernelGGL(sp.ns1 <= 4 * kMergeMax ? score_rowmerge_kernel<true> : score_rowmerge_kernel<false>,
+                     dim3((rows_total + 63) / 64), dim3(256), 0, stream, rows_total, d.R, sp.ns1, rowpart, rowstat);
+  if (sp.n_vt > 0) {
     hipLaunchKernelGGL((score_colmass_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_vt, sp.rs2)),
-                       dim3(256), 0, stream, d, a.q, a.k, a.token_keep, rowstat, colpart);
-  if (sp.n_vt > 0)
-    hipLaunchKernelGGL(score_colsum_kernel, dim3(sp.n_vt, a.B), dim3(256), 0, stream, a.S, a.V_full,
-                       a.Hkv * sp.rs2, (float)a.Hq * (float)d.T, colpart, a.token_keep, a.scores);
+                       dim3(64 * kColWaves), 0, stream, d, a.q, a.k, a.token_keep, rowstat, colpart);
+    hipLaunchKernelGGL(score_colsum_kernel, dim3((a.V_full + 255) / 256, a.B), dim3(256), 0, stream, a.S,
+                       a.V_full, a.Hkv * sp.rs2, (float)a.Hq * (float)d.T, colpart, a.token_keep, a.scores);
+  }
 }
 
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
@@ -1019,10 +1301,11 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.Hkv = a.Hkv;
   d.G = a.Hq / a.Hkv;
   d.R = d.G * d.T;
-  d.nchunks = sp.nchunks;
+  d.n_rb = sp.n_rb;
   d.n_kt = sp.n_kt;
+  d.ns1 = sp.ns1;
   d.n_vt = sp.n_vt;
-  d.rs1 = sp.rs1;
+  d.nchunks = sp.nchunks;
   d.rs2 = sp.rs2;
   d.scale_log2 = a.logit_scale_log2;
 
