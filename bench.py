@@ -9,8 +9,9 @@ heads, head dim 128, bf16, batch 1) at keep ratio 0.5; the keep-ratio sweep
 
 Prints ONE JSON line. Inputs are seeded synthetic tensors already resident in
 HBM; the timed steps rotate over several input sets whose total exceeds the
-256 MB last-level cache. Per-kernel durations come from HIP events recorded
-on the launch stream around each call inside the timed region.
+256 MB last-level cache. The headline steps are timed with events only around
+the whole timed region; per-call durations come from a second pass of the same
+steps with HIP events recorded on the launch stream around each call.
 """
 from __future__ import annotations
 
@@ -276,7 +277,7 @@ def main():
                        "prefill_attn": round(attn_us, 2)},
         "select_stage": {"score_gflop": round(sel_flops / 1e9, 3),
                          "gather_mb": round(gbytes / 1e6, 2)},
-        "roofline": {"bound": "mfma", "kernel": "attn_fwd_bf16_kernel",
+        "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel",
                      "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "flop_per_launch": fl},
