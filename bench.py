@@ -190,6 +190,34 @@ def main():
             cu = self.outs["cu_seqlens"].cpu().numpy()
             return total_ms / steps, per.mean(axis=0), cu
 
+        def measure_graph(self, r, steps, warmup):
+            """ms per step with each input set's step (the three calls) captured
+            once in a HIP graph and the graphs replayed in rotation."""
+            graphs = []
+            for st in self.sets:
+                side = torch.cuda.Stream()
+                side.wait_stream(torch.cuda.current_stream())
+                with torch.cuda.stream(side):
+                    self.step(st, r)  # first use of the capture pool and the library on this stream
+                torch.cuda.current_stream().wait_stream(side)
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g):
+                    self.step(st, r)
+                graphs.append(g)
+            for i in range(warmup):
+                graphs[i % len(graphs)].replay()
+            torch.cuda.synchronize()
+            t0 = torch.cuda.Event(enable_timing=True)
+            t1 = torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            for i in range(steps):
+                graphs[i % len(graphs)].replay()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            ms = t0.elapsed_time(t1) / steps
+            del graphs
+            return ms
+
     if args.workload == 3:
         main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])
     else:
@@ -201,6 +229,7 @@ def main():
     measure = main_runner.measure
 
     ms_step, per, cu = measure(args.keep_ratio, args.steps, args.warmup)
+    ms_graph = main_runner.measure_graph(args.keep_ratio, args.steps, args.warmup)
     seqlens = np.diff(cu).tolist()
     fl = attn_flops(seqlens, Hq, D)
     attn_us = per[2] * 1e3
@@ -271,6 +300,8 @@ def main():
                    "global_batch": B, "seq_len": S, "compacted_len": seqlens,
                    "keep_ratio": args.keep_ratio, "parallelism": "none (1 GPU)",
                    "input_sets_rotated": args.sets},
+        "hip_graph": {"ms_per_step": round(ms_graph, 4),
+                      "note": "the same steps with each input set's three calls captured in one HIP graph"},
         "prefill_attn_tflops": round(attn_tflops, 1),
         "kernels_us": {"patch_select": round(per[0] * 1e3, 2),
                        "token_score_topk_gather": round(per[1] * 1e3, 2),

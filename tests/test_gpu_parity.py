@@ -198,6 +198,59 @@ def test_chain_is_deterministic():
     assert torch.equal(oa[:a["cu"][-1]].view(torch.int16), ob[:a["cu"][-1]].view(torch.int16))
 
 
+def test_graph_replay_matches_eager():
+    """The step's three calls captured in one HIP graph: every replay, with eager
+    work (the outputs cleared) and a sync between replays, reproduces the eager
+    results bit for bit."""
+    case = synth.config_case(4, Tv=128, T=32)
+    B, S, Hq, Hkv, D, V = case.B, case.S, case.Hq, case.Hkv, case.D, case.V_full
+    q, k, v = (to_device(x, case.dtype) for x in (case.q, case.k, case.v))
+    logit = torch.from_numpy(case.view_logit).cuda()
+    out = dict(scores=torch.empty((B, V), dtype=torch.float32, device="cuda"),
+               kept_index=torch.empty((B * S,), dtype=torch.int32, device="cuda"),
+               cu_seqlens=torch.empty((B + 1,), dtype=torch.int32, device="cuda"),
+               qc=torch.empty((B * S, Hq, D), dtype=q.dtype, device="cuda"),
+               kc=torch.empty((B * S, Hkv, D), dtype=q.dtype, device="cuda"),
+               vc=torch.empty((B * S, Hkv, D), dtype=q.dtype, device="cuda"),
+               workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D),), dtype=torch.uint8,
+                                     device="cuda"))
+    o = torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device="cuda")
+
+    def step():
+        _, tk, _ = lv.patch_select(logit, case.view_offsets, S, case.w_lexical, case.threshold)
+        lv.token_score_topk(q, k, v, tk, case.keep_ratio, V, q_scale=case.q_scale, k_scale=case.k_scale,
+                            v_scale=case.v_scale, out=out)
+        lv.prefill_attn(out["qc"], out["kc"], out["vc"], out["cu_seqlens"], S, B=B, q_scale=case.q_scale,
+                        k_scale=case.k_scale, v_scale=case.v_scale, out=o)
+
+    step()
+    torch.cuda.synchronize()
+    total = int(out["cu_seqlens"][-1])
+    names = ("scores", "kept_index", "cu_seqlens", "qc", "kc", "vc")
+    rows = {"kept_index": total, "qc": total, "kc": total, "vc": total}
+    ref = {n: out[n][:rows.get(n, out[n].shape[0])].clone() for n in names}
+    ref_o = o[:total].clone()
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step()
+    for rep in range(3):
+        for t in list(out.values()) + [o]:
+            t.zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for n in names:
+            got = out[n][:rows.get(n, out[n].shape[0])]
+            assert torch.equal(got.view(torch.uint8), ref[n].view(torch.uint8)), f"replay {rep}: {n}"
+        assert torch.equal(o[:total].view(torch.int16), ref_o.view(torch.int16)), f"replay {rep}: o"
+    log(f"graph replays: 3 x bitwise equal to eager ({total} packed rows)")
+
+
 def test_full_keep_equals_unpruned_attention():
     case = synth.config_case(2, Tv=64, T=16, keep_ratio=1.0, n_masked=0)
     g = run_select(case)
