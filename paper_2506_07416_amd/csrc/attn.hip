@@ -32,6 +32,26 @@ struct AttnParams {
   float scale_log2, out_scale;
 };
 
+// max(a, b, c): the NaN-propagating maximum, which folds into one
+// v_maximum3_f32 (no canonicalisation).
+__device__ __forceinline__ float max3f(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
+}
+
+// Maximum of the 32 accumulator values s[0][0..15], s[1][0..15] as a tree of
+// 16 three-input maxima, depth 4.
+__device__ __forceinline__ float max32(const f32x16 s[2]) {
+  float t[11];
+#pragma unroll
+  for (int i = 0; i < 10; ++i) {
+    const int a = 3 * i, b = 3 * i + 1, c = 3 * i + 2;
+    t[i] = max3f(s[a >> 4][a & 15], s[b >> 4][b & 15], s[c >> 4][c & 15]);
+  }
+  t[10] = max3f(s[1][14], s[1][15], t[9]);
+  const float u0 = max3f(t[0], t[1], t[2]), u1 = max3f(t[3], t[4], t[5]), u2 = max3f(t[6], t[7], t[8]);
+  return max3f(u0, u1, __builtin_elementwise_maximum(u2, t[10]));
+}
+
 // Row of the 32x32 accumulator held in register r by lane half hl.
 __device__ __forceinline__ int acc_row32(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
 // Swap bits 2 and 3: the K-row order that lines S^T up with the P.V operand.
@@ -133,16 +153,19 @@ attn_bf16_kernel(AttnParams p) {
   const int wave_q0 = m0 + w * 32;
 
   // ---- per-lane constants
+  // Copy j of a wave moves 16-byte pieces of tile row ld_row[j]; its source
+  // is (tile base, wave-uniform) + ld_koff[j] / ld_voff[j] (per lane, fixed).
   int ld_row[LI];
-  uint32_t ld_kpiece[LI], ld_vpiece[LI];
+  uint32_t ld_koff[LI], ld_voff[LI];
 #pragma unroll
   for (int j = 0; j < LI; ++j) {
     const int slot = (w + NW * j) * 64 + lane;
     const int r = slot / NP, ph = slot % NP;
     ld_row[j] = r;
-    ld_kpiece[j] = (uint32_t)(ph ^ (r & (NP - 1))) * 16;
-    ld_vpiece[j] = (uint32_t)(ph ^ (4 * (r & VSW))) * 16;
+    ld_koff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ (r & (NP - 1))) * 16;
+    ld_voff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ (4 * (r & VSW))) * 16;
   }
+  const uint32_t lds_w = __builtin_amdgcn_readfirstlane((uint32_t)w * 1024u);  // this wave's copy slot
   // K operand of S^T block nb: row 32*nb + swap23(lq), logical piece 2*ks + hl
   const int rho = swap23(lq);
   uint32_t koff[KS];
@@ -160,18 +183,21 @@ attn_bf16_kernel(AttnParams p) {
     voff[db] = vrow0 * RB + (((c0 >> 1) ^ (4 * (vrow0 & VSW))) * 16) + (c0 & 1) * 8;
   }
 
-  auto copy_tile = [&](int tile, int buf) {
+  auto copy_tile = [&](int tile, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
     const int k0 = tile * BN;
+    const uint8_t* kt = kbase + (size_t)k0 * kvrow;
+    const uint8_t* vt = vbase + (size_t)k0 * kvrow;
     const bool full = k0 + BN <= len;
 #pragma unroll
     for (int j = 0; j < LI; ++j) {
-      const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
-      const uint32_t ro = (uint32_t)key * kvrow;
-      __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(kvl + buf * TB + (w + NW * j) * 1024),
+      // rows past the sequence end repeat its last key
+      const uint32_t fix = full ? 0u : (uint32_t)(min(k0 + ld_row[j], len - 1) - (k0 + ld_row[j])) * kvrow;
+      __builtin_amdgcn_global_load_lds((const void*)(kt + (ld_koff[j] + fix)),
+                                       (__attribute__((address_space(3))) void*)(kvl + BUF * TB + lds_w + NW * j * 1024),
                                        16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(kvl + (2 + buf) * TB + (w + NW * j) * 1024),
+      __builtin_amdgcn_global_load_lds((const void*)(vt + (ld_voff[j] + fix)),
+                                       (__attribute__((address_space(3))) void*)(kvl + (2 + BUF) * TB + lds_w + NW * j * 1024),
                                        16, 0, 0);
     }
   };
@@ -193,19 +219,21 @@ attn_bf16_kernel(AttnParams p) {
   const int kend = CAUSAL ? min(len, m0 + BM) : len;
   const int nt = (kend + BN - 1) / BN;
 
-  copy_tile(0, 0);
+  copy_tile(0, std::integral_constant<int, 0>{});
   wait_vmcnt<0>();
   __syncthreads();
 
-  for (int t = 0; t < nt; ++t) {
-    const int buf = t & 1;
+  // step t (K, V of tile t in buffers BUF = t & 1); instantiated per buffer so
+  // that every LDS offset is an immediate
+  auto step = [&](int t, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
     const int k0 = t * BN;
-    if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);   // buffer last read in step t-1
+    if (t + 1 < nt) copy_tile(t + 1, std::integral_constant<int, BUF ^ 1>{});  // buffer last read in step t-1
     if (!(CAUSAL && k0 > wave_q0 + 31)) {
       // ---- S^T blocks: 2 x (32 keys x 32 queries). K operands are read from
       // LDS two k-steps ahead of their MFMAs (a ring of three).
-      const uint8_t* kl = kvl + buf * TB;
-      const uint8_t* vl = kvl + (2 + buf) * TB;
+      const uint8_t* kl = kvl + BUF * TB;
+      const uint8_t* vl = kvl + (2 + BUF) * TB;
       f32x16 s[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -254,10 +282,11 @@ attn_bf16_kernel(AttnParams p) {
             if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
           }
       }
-      float mx = __builtin_elementwise_maximum(s[0][0], s[1][0]);
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = __builtin_elementwise_maximum(mx, __builtin_elementwise_maximum(s[0][r], s[1][r]));
-      mx = max_xor32(mx);
+      float mx = max32(s);
+      {
+        const float2 pr = pair_xor32(mx);
+        mx = __builtin_elementwise_maximum(pr.x, pr.y);
+      }
       // ---- lazy rescale
       const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
       if (__any(grow)) {
@@ -272,20 +301,18 @@ attn_bf16_kernel(AttnParams p) {
       }
       const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
       // ---- P = exp2(s*c - m*c) as the B operand of O^T += V^T P^T
-      float rs = 0.f;
+      float rsk[4];
       bf16x8 pb[4];
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
         float e[8];
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          e[i] = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][8 * (kk & 1) + i], c, -mc));
-          rs += e[i];
-        }
+        for (int i = 0; i < 8; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][8 * (kk & 1) + i], c, -mc));
         pb[kk] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
                         (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
+        rsk[kk] = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
       }
-      l_run += rs;
+      l_run += (rsk[0] + rsk[1]) + (rsk[2] + rsk[3]);
       // ---- O^T += V^T P^T; V operands one k-step ahead of their MFMAs
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
@@ -309,6 +336,10 @@ attn_bf16_kernel(AttnParams p) {
     }
     wait_vmcnt<0>();
     __syncthreads();
+  };
+  for (int t = 0; t < nt; t += 2) {
+    step(t, std::integral_constant<int, 0>{});
+    if (t + 1 < nt) step(t + 1, std::integral_constant<int, 1>{});
   }
 
   const float l = sum_xor32(l_run);
