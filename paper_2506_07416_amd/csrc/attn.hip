@@ -408,16 +408,19 @@ attn_fp8_kernel(AttnParams p) {
   };
   auto vswz = [](int r) { return (r >> 1) & (NP - 1) & 3; };
 
+  // Copy j of a wave moves 16-byte pieces of tile row ld_row[j]; its source
+  // is (tile base, wave-uniform) + ld_koff[j] / ld_voff[j] (per lane, fixed).
   int ld_row[LI];
-  uint32_t ld_kpiece[LI], ld_vpiece[LI];
+  uint32_t ld_koff[LI], ld_voff[LI];
 #pragma unroll
   for (int j = 0; j < LI; ++j) {
     const int slot = min(w + NW * j, NI - 1) * 64 + lane;
     const int r = slot / NP, ph = slot % NP;
     ld_row[j] = r;
-    ld_kpiece[j] = (uint32_t)(ph ^ kswz(r)) * 16;
-    ld_vpiece[j] = (uint32_t)(ph ^ vswz(r)) * 16;
+    ld_koff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ kswz(r)) * 16;
+    ld_voff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ vswz(r)) * 16;
   }
+  const uint32_t lds_w = __builtin_amdgcn_readfirstlane((uint32_t)w * 1024u);  // this wave's copy slot
   // K operand: rows tile_key<fp8>(nb, lq), pieces 4*ks + 2*hl and +1
   uint32_t koff[2][QKS][2];
 #pragma unroll
@@ -437,19 +440,22 @@ attn_fp8_kernel(AttnParams p) {
     voff[db] = vrow0 * RB + (((2 * db + (g16 & 1)) ^ vswz(vrow0)) * 16) + (s16 & 1) * 8;
   // rows vrow0 + 8*j share vswz: (r>>1)&3 depends on bits 1,2 only
 
-  auto copy_tile = [&](int tile, int buf) {
+  auto copy_tile = [&](int tile, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
     const int k0 = tile * BN;
+    const uint8_t* kt = kbase + (size_t)k0 * kvrow;
+    const uint8_t* vt = vbase + (size_t)k0 * kvrow;
     const bool full = k0 + BN <= len;
 #pragma unroll
     for (int j = 0; j < LI; ++j) {
       if (w + NW * j >= NI) break;
-      const int key = full ? k0 + ld_row[j] : min(k0 + ld_row[j], len - 1);
-      const uint32_t ro = (uint32_t)key * kvrow;
-      __builtin_amdgcn_global_load_lds((const void*)(kbase + ro + ld_kpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(kvl + buf * TB + (w + NW * j) * 1024),
+      // rows past the sequence end repeat its last key
+      const uint32_t fix = full ? 0u : (uint32_t)(min(k0 + ld_row[j], len - 1) - (k0 + ld_row[j])) * kvrow;
+      __builtin_amdgcn_global_load_lds((const void*)(kt + (ld_koff[j] + fix)),
+                                       (__attribute__((address_space(3))) void*)(kvl + BUF * TB + lds_w + NW * j * 1024),
                                        16, 0, 0);
-      __builtin_amdgcn_global_load_lds((const void*)(vbase + ro + ld_vpiece[j]),
-                                       (__attribute__((address_space(3))) void*)(kvl + (2 + buf) * TB + (w + NW * j) * 1024),
+      __builtin_amdgcn_global_load_lds((const void*)(vt + (ld_voff[j] + fix)),
+                                       (__attribute__((address_space(3))) void*)(kvl + (2 + BUF) * TB + lds_w + NW * j * 1024),
                                        16, 0, 0);
     }
   };
@@ -474,16 +480,18 @@ attn_fp8_kernel(AttnParams p) {
   const int kend = CAUSAL ? min(len, m0 + BM) : len;
   const int nt = (kend + BN - 1) / BN;
 
-  copy_tile(0, 0);
+  copy_tile(0, std::integral_constant<int, 0>{});
   wait_vmcnt<0>();
   __syncthreads();
 
-  for (int t = 0; t < nt; ++t) {
-    const int buf = t & 1;
+  // step t (K, V of tile t in buffers BUF = t & 1); instantiated per buffer so
+  // that every LDS offset is an immediate
+  auto step = [&](int t, auto bufc) __attribute__((always_inline)) {
+    constexpr int BUF = decltype(bufc)::value;
     const int k0 = t * BN;
-    if (t + 1 < nt) copy_tile(t + 1, buf ^ 1);
+    if (t + 1 < nt) copy_tile(t + 1, std::integral_constant<int, BUF ^ 1>{});
     if (!(CAUSAL && k0 > wave_q0 + 31)) {
-      const uint8_t* kl = kvl + buf * TB;
+      const uint8_t* kl = kvl + BUF * TB;
       f32x16 s[2];
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
@@ -509,10 +517,11 @@ attn_fp8_kernel(AttnParams p) {
             if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
           }
       }
-      float mx = fmaxf(s[0][0], s[1][0]);
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, fmaxf(s[0][r], s[1][r]));
-      mx = max_xor32(mx);
+      float mx = max32(s);
+      {
+        const float2 pr = pair_xor32(mx);
+        mx = __builtin_elementwise_maximum(pr.x, pr.y);
+      }
       // exact running max: rescale whenever it grows
       const bool grow = mx > m_run;
       if (__any(grow)) {
@@ -527,23 +536,21 @@ attn_fp8_kernel(AttnParams p) {
       }
       // p * 2^PSHIFT = exp2(s*c - m*c + PSHIFT)
       const float mc = (m_run == -INFINITY) ? 0.f : m_run * c - (float)PSHIFT;
-      float rs = 0.f;
+      float rsi[8];
       int pw[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
         const int nb = i >> 2, r0 = (i & 3) * 4;
         float e[4];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          e[u] = __builtin_amdgcn_exp2f(fmaf(s[nb][r0 + u], c, -mc));
-          rs += e[u];
-        }
+        for (int u = 0; u < 4; ++u) e[u] = __builtin_amdgcn_exp2f(fmaf(s[nb][r0 + u], c, -mc));
+        rsi[i] = (e[0] + e[1]) + (e[2] + e[3]);
         int wd = __builtin_amdgcn_cvt_pk_fp8_f32(e[0], e[1], 0, false);
         pw[i] = __builtin_amdgcn_cvt_pk_fp8_f32(e[2], e[3], wd, true);
       }
-      l_run += rs;
+      l_run += ((rsi[0] + rsi[1]) + (rsi[2] + rsi[3])) + ((rsi[4] + rsi[5]) + (rsi[6] + rsi[7]));
       const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
-      const uint8_t* vl = kvl + (2 + buf) * TB;
+      const uint8_t* vl = kvl + (2 + BUF) * TB;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
         i32x2 part[4];
@@ -557,6 +564,10 @@ attn_fp8_kernel(AttnParams p) {
     }
     wait_vmcnt<0>();
     __syncthreads();
+  };
+  for (int t = 0; t < nt; t += 2) {
+    step(t, std::integral_constant<int, 0>{});
+    if (t + 1 < nt) step(t + 1, std::integral_constant<int, 1>{});
   }
 
   const float l = sum_xor32(l_run);
