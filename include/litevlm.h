@@ -62,6 +62,7 @@ typedef enum {
 #define LITEVLM_MAX_VIEWS 64      /* N */
 #define LITEVLM_MAX_VISUAL 16384  /* V_full (top-k keeps every key of a sample in LDS) */
 #define LITEVLM_MAX_BATCH 256     /* B */
+#define LITEVLM_MAX_HEADS 128     /* Hq (the gather copies a token's Q, K, V rows in one pass) */
 
 /* Library version as major*10000 + minor*100 + patch. */
 int32_t litevlm_version(void);
@@ -127,7 +128,8 @@ size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full,
  *
  *   dtype              LITEVLM_F32, LITEVLM_BF16 or LITEVLM_FP8_E4M3 (Q, K, V, qc, kc, vc)
  *   B, S, V_full       batch (1..LITEVLM_MAX_BATCH), sequence length, visual tokens (T = S - V_full >= 1)
- *   Hq, Hkv, D         query heads, KV heads (Hq % Hkv == 0), head dim (64 or 128)
+ *   Hq, Hkv, D         query heads (1..LITEVLM_MAX_HEADS), KV heads (Hq % Hkv == 0),
+ *                      head dim (64 or 128)
  *   q                  dev [B, S, Hq, D]
  *   k                  dev [B, S, Hkv, D]
  *   v                  dev [B, S, Hkv, D] (may be NULL when vc is NULL)

@@ -14,7 +14,7 @@ LIB_PATH = os.path.join(HERE, "liblitevlm.so")
 OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_VALUE, ERR_UNSUPPORTED, ERR_MISALIGNED, \
     ERR_WORKSPACE, ERR_HIP = range(8)
 F32, BF16, FP8_E4M3 = 0, 1, 2
-MAX_VIEWS, MAX_VISUAL, MAX_BATCH = 64, 16384, 256
+MAX_VIEWS, MAX_VISUAL, MAX_BATCH, MAX_HEADS = 64, 16384, 256, 128
 
 # Every symbol the header declares, with its C signature.
 _vp, _i32, _f32, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_double, ctypes.c_size_t

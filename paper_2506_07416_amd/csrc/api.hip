@@ -21,7 +21,7 @@ litevlm_status_t check_score_shape(int32_t B, int32_t S, int32_t V_full, int32_t
                                    int32_t D) {
   if (B < 1 || B > LITEVLM_MAX_BATCH) return LITEVLM_ERR_BAD_SHAPE;
   if (V_full < 0 || V_full > LITEVLM_MAX_VISUAL || S <= V_full) return LITEVLM_ERR_BAD_SHAPE;
-  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0) return LITEVLM_ERR_BAD_SHAPE;
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv != 0 || Hq > LITEVLM_MAX_HEADS) return LITEVLM_ERR_BAD_SHAPE;
   if (D != 64 && D != 128) return LITEVLM_ERR_BAD_SHAPE;
   // keep every index computed in int32 inside range
   if ((int64_t)B * S * Hq * D > ((int64_t)1 << 40)) return LITEVLM_ERR_BAD_SHAPE;

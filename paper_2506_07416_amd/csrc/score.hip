@@ -108,13 +108,15 @@ struct RowTileBf16 {
   // each 16-lane group reads 16 rows x 1 piece: conflict-free
   __device__ __forceinline__ static int swz(int key) { return key & (NP - 1); }
 
-  // k-step ks of lane half hl holds head dims 16*ks + 8*hl .. +7
-  __device__ __forceinline__ void init(const QRows& qr, int row, int lane) {
+  static constexpr bool QSTAGE = true;  // query rows arrive through an LDS stage
+
+  // k-step ks of lane half hl holds head dims 16*ks + 8*hl .. +7, read from a
+  // staged row (pieces swizzled by swz of the row's index in the stage)
+  __device__ __forceinline__ void init_lds(const uint8_t* stage, int srow, int lane) {
     const int lq = lane & 31, hl = lane >> 5;
-    const uint8_t* p = qr.row(row);
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)
-      q[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(p + (2 * ks + hl) * 16));
+      q[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(stage + srow * RB + ((2 * ks + hl) ^ swz(srow)) * 16));
     kbase = lq * RB + (hl ^ swz(lq)) * 16;  // key 32*nb + lq adds 32*nb*RB
   }
 
@@ -159,15 +161,17 @@ struct RowTileFp8 {
   // rows 2i, 2i+1 fill 16 banks-groups between them: conflict-free
   __device__ __forceinline__ static int swz(int key) { return (key >> 1) & (NP - 1); }
 
-  // k-step ks of lane half hl holds bytes 64*ks + 32*hl .. +31
-  __device__ __forceinline__ void init(const QRows& qr, int row, int lane) {
+  static constexpr bool QSTAGE = true;  // query rows arrive through an LDS stage
+
+  // k-step ks of lane half hl holds bytes 64*ks + 32*hl .. +31 of a staged row
+  __device__ __forceinline__ void init_lds(const uint8_t* stage, int srow, int lane) {
     const int lq = lane & 31, hl = lane >> 5;
-    const uint8_t* p = qr.row(row);
+    const uint8_t* p = stage + srow * RB;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int piece = 4 * ks + 2 * hl;
-      const u32x4 lo = *reinterpret_cast<const u32x4*>(p + piece * 16);
-      const u32x4 hi = *reinterpret_cast<const u32x4*>(p + piece * 16 + 16);
+      const u32x4 lo = *reinterpret_cast<const u32x4*>(p + ((piece ^ swz(srow)) * 16));
+      const u32x4 hi = *reinterpret_cast<const u32x4*>(p + (((piece + 1) ^ swz(srow)) * 16));
       q[ks] = i32x8{(int)lo[0], (int)lo[1], (int)lo[2], (int)lo[3], (int)hi[0], (int)hi[1], (int)hi[2], (int)hi[3]};
 #pragma unroll
       for (int hp = 0; hp < 2; ++hp) koff[2 * ks + hp] = lq * RB + ((piece + hp) ^ swz(lq)) * 16;
@@ -202,8 +206,9 @@ struct RowTileF32 {
   static constexpr int NP = RB / 16;
   static constexpr int TILE = KB * RB;
   static constexpr int NBUF = TILE >= 32768 ? 3 : 4;  // LDS budget of the 32 KB fp32 tiles
+  static constexpr bool QSTAGE = false;  // query rows are read from global memory in logits
   __device__ __forceinline__ static int swz(int) { return 0; }
-  __device__ __forceinline__ void init(const QRows&, int, int) {}
+  __device__ __forceinline__ void init_lds(const uint8_t*, int, int) {}
 
   // row0: the wave's first query row
   __device__ __forceinline__ void logits(const uint8_t* kl, f32x16 s[2], const QRows& qr, int row0, int lane) const {
@@ -359,12 +364,20 @@ __global__ void __launch_bounds__(kSweepThreads)
 score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                       const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
   using Tile = typename RowTileOf<DT, D>::T;
-  // One LDS object (key ring, keep bytes, flag words): with a single object
-  // the compiler adds no vmcnt wait of its own before reads of one buffer
-  // while direct copies into another are in flight; the explicit waits and
-  // barriers order copies before reads.
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tile::NBUF * Tile::TILE + kMaxSplitTiles * KB + 2 * kSweepWaves * 8];
-  uint8_t* keepl = lds + Tile::NBUF * Tile::TILE;
+  // The workgroup's query rows pass through a 64 KB stage in rounds of QRR
+  // rows (whole rows per 1 KB direct copy, so every copy reads contiguous
+  // bytes), and each wave then reads its operand registers from the stage.
+  constexpr int QST = Tile::QSTAGE ? 65536 : 0;
+  constexpr int QRR = Tile::QSTAGE ? QST / Tile::RB : 1;
+  constexpr int NQR = Tile::QSTAGE ? (RBLK * Tile::RB + QST - 1) / QST : 0;
+  static_assert(!Tile::QSTAGE || (QST % Tile::RB == 0 && (QRR % 32) == 0), "stage rounds must hold whole waves");
+  // One LDS object (key ring, query stage, keep bytes, flag words): with a
+  // single object the compiler adds no vmcnt wait of its own before reads of
+  // one buffer while direct copies into another are in flight; the explicit
+  // waits and barriers order copies before reads.
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tile::NBUF * Tile::TILE + QST + kMaxSplitTiles * KB + 2 * kSweepWaves * 8];
+  uint8_t* qstage = lds + Tile::NBUF * Tile::TILE;
+  uint8_t* keepl = qstage + QST;
   uint64_t* mw = reinterpret_cast<uint64_t*>(keepl + kMaxSplitTiles * KB);
 
   int col, split;
@@ -383,15 +396,46 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   const int row = row0 + lq;
   const bool wave_active = row0 < d.R;
 
-  // keep bytes, the wave's query rows and the first NBUF-1 key tiles, all in flight together
+  // copies of query-row round `round` into the stage: row rr of the round,
+  // 16-byte piece ph at stage slot ph ^ swz(rr)
+  auto q_round = [&](int round) {
+    const int ncopy = min(QRR, RBLK - round * QRR) * Tile::RB / 1024;
+    for (int sub = w; sub < ncopy; sub += kSweepWaves) {
+      const int slot = sub * 64 + lane;
+      const int rr = slot / Tile::NP, ph = slot - rr * Tile::NP;
+      __builtin_amdgcn_global_load_lds((const void*)(qr.row(rb * RBLK + round * QRR + rr) + (ph ^ Tile::swz(rr)) * 16),
+                                       (__attribute__((address_space(3))) void*)(qstage + sub * 1024), 16, 0, 0);
+    }
+  };
+  const int my_round = (32 * w) / QRR, srow = 32 * w + lq - my_round * QRR;
+
+  // keep bytes, the first query round and the first NBUF-1 key tiles, all in flight together
   uint8_t kf[kFlagsPer];
   load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
+  if (Tile::QSTAGE) q_round(0);
   Tile tile;
-  if (wave_active) tile.init(qr, row, lane);
   KeyPipe<Tile> pipe(lds, k + ((size_t)b * d.S * d.Hkv + g) * Tile::RB, (size_t)d.Hkv * Tile::RB, tile0, ntl,
                      d.S, w, lane);
 #pragma unroll
   for (int t = 0; t < Tile::NBUF - 1; ++t) pipe.issue(t);
+  if (Tile::QSTAGE) {
+    // round 0 has landed once at most the key copies issued after it remain
+    switch (min(Tile::NBUF - 1, ntl) * pipe.cpw) {
+      case 0: wait_vmcnt<0>(); break;
+      case 1: wait_vmcnt<1>(); break;
+      case 2: wait_vmcnt<2>(); break;
+      default: wait_vmcnt<3>(); break;
+    }
+    __syncthreads();
+    if (wave_active && my_round == 0) tile.init_lds(qstage, srow, lane);
+    for (int round = 1; round < NQR; ++round) {
+      __syncthreads();  // every read of the previous round is done
+      q_round(round);
+      wait_vmcnt<0>();
+      __syncthreads();
+      if (wave_active && my_round == round) tile.init_lds(qstage, srow, lane);
+    }
+  }
   pipe.wait_for(0);
   __syncthreads();  // tile 0 and the keep bytes have landed
   uint64_t live, plain;
@@ -1162,67 +1206,76 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
 }
 
 // ---------------------------------------------------------------- gather
-// Each workgroup copies kGatherRows packed rows per iteration: the source
-// rows are resolved first, then every 16-byte load of the group is issued
-// (from clamped, always-valid addresses) before the predicated stores.
-
-constexpr int kGatherRows = 4;
+// Each packed row is one token's Q, K and V rows, W = qvec + 2*kvvec 16-byte
+// pieces; thread t copies pieces t, t+256, ... of every row, so no thread idles
+// on the short K/V rows. A workgroup takes RPI rows per iteration: the
+// kept indices are loaded together with cu_seqlens (they need no offset), the
+// sample of each row is found by a search of cu_seqlens in LDS, then every
+// 16-byte load of the group is issued (from clamped, always-valid addresses)
+// before the predicated stores.
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-template <int QPT, int KPT>
+template <int PPT, int RPI>
 __global__ void __launch_bounds__(256)
 gather_rows_kernel(int B, int S, const int32_t* __restrict__ kept_index,
                    const int32_t* __restrict__ cu_seqlens, const u32x4* __restrict__ q,
                    const u32x4* __restrict__ k, const u32x4* __restrict__ v, u32x4* __restrict__ qc,
                    u32x4* __restrict__ kc, u32x4* __restrict__ vc, int qvec, int kvvec) {
   __shared__ int cu[LITEVLM_MAX_BATCH + 1];
-  for (int i = threadIdx.x; i <= B; i += blockDim.x) cu[i] = cu_seqlens[i];
+  const int tid = threadIdx.x;
+  const int cap = B * S;
+  // segment and offset of this thread's pieces (the same for every row)
+  int seg[PPT], off[PPT];
+#pragma unroll
+  for (int j = 0; j < PPT; ++j) {
+    const int p = tid + 256 * j;
+    seg[j] = p < qvec ? 0 : (p < qvec + kvvec ? 1 : (p < qvec + 2 * kvvec ? 2 : 3));
+    off[j] = seg[j] == 0 ? p : (seg[j] == 1 ? p - qvec : p - qvec - kvvec);
+    if ((seg[j] == 0 && !qc) || (seg[j] == 1 && !kc) || (seg[j] == 2 && !vc)) seg[j] = 3;  // not requested
+  }
+  int base = blockIdx.x * RPI;
+  int idx[RPI];
+#pragma unroll
+  for (int r = 0; r < RPI; ++r) idx[r] = kept_index[min(base + r, cap - 1)];
+  for (int i = tid; i <= B; i += blockDim.x) cu[i] = cu_seqlens[i];
   __syncthreads();
   const int total = cu[B];
-  const int tid = threadIdx.x;
-  for (int base = blockIdx.x * kGatherRows; base < total; base += gridDim.x * kGatherRows) {
-    size_t src[kGatherRows];
+  for (; base < total; base += gridDim.x * RPI) {
+    size_t src[RPI];
 #pragma unroll
-    for (int r = 0; r < kGatherRows; ++r) {
+    for (int r = 0; r < RPI; ++r) {
       const int i = min(base + r, total - 1);
       // last b with cu[b] <= i, by a fixed 8-step search (B <= 256)
       int lo = 0;
 #pragma unroll
       for (int step = 128; step >= 1; step >>= 1)
         if (lo + step <= B - 1 && cu[lo + step] <= i) lo += step;
-      src[r] = (size_t)lo * S + kept_index[i];
+      src[r] = (size_t)lo * S + (base + r < total ? idx[r] : idx[0]);
     }
-    u32x4 qv[kGatherRows * QPT], kv[kGatherRows * KPT], vv[kGatherRows * KPT];
+    // indices of the next iteration, in flight with this one's rows
+    const int nbase = base + gridDim.x * RPI;
+    if (nbase < total) {
 #pragma unroll
-    for (int r = 0; r < kGatherRows; ++r) {
-      // kernel-uniform guards: an input is only read when its copy is requested
+      for (int r = 0; r < RPI; ++r) idx[r] = kept_index[min(nbase + r, cap - 1)];
+    }
+    u32x4 val[RPI][PPT];
 #pragma unroll
-      for (int j = 0; j < QPT; ++j) {
-        const int c = min(tid + 256 * j, qvec - 1);
-        if (qc) qv[r * QPT + j] = q[src[r] * qvec + c];
+    for (int r = 0; r < RPI; ++r)
+#pragma unroll
+      for (int j = 0; j < PPT; ++j) {
+        const u32x4* sp = seg[j] == 0 ? q + src[r] * qvec : (seg[j] == 1 ? k + src[r] * kvvec : v + src[r] * kvvec);
+        if (seg[j] != 3) val[r][j] = sp[off[j]];
       }
 #pragma unroll
-      for (int j = 0; j < KPT; ++j) {
-        const int c = min(tid + 256 * j, kvvec - 1);
-        if (kc) kv[r * KPT + j] = k[src[r] * kvvec + c];
-        if (vc) vv[r * KPT + j] = v[src[r] * kvvec + c];
-      }
-    }
-#pragma unroll
-    for (int r = 0; r < kGatherRows; ++r) {
+    for (int r = 0; r < RPI; ++r) {
       const int i = base + r;
-      const bool row_ok = i < total;
+      if (i >= total) continue;
 #pragma unroll
-      for (int j = 0; j < QPT; ++j) {
-        const int c = tid + 256 * j;
-        if (qc && row_ok && c < qvec) qc[(size_t)i * qvec + c] = qv[r * QPT + j];
-      }
-#pragma unroll
-      for (int j = 0; j < KPT; ++j) {
-        const int c = tid + 256 * j;
-        if (kc && row_ok && c < kvvec) kc[(size_t)i * kvvec + c] = kv[r * KPT + j];
-        if (vc && row_ok && c < kvvec) vc[(size_t)i * kvvec + c] = vv[r * KPT + j];
+      for (int j = 0; j < PPT; ++j) {
+        if (seg[j] == 0) qc[(size_t)i * qvec + off[j]] = val[r][j];
+        else if (seg[j] == 1) kc[(size_t)i * kvvec + off[j]] = val[r][j];
+        else if (seg[j] == 2) vc[(size_t)i * kvvec + off[j]] = val[r][j];
       }
     }
   }
@@ -1323,22 +1376,27 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
     const int esz = a.dtype == LITEVLM_F32 ? 4 : (a.dtype == LITEVLM_BF16 ? 2 : 1);
     const int qvec = a.Hq * a.D * esz / 16, kvvec = a.Hkv * a.D * esz / 16;
     const int rows = a.B * a.S;
-    const int grid = std::max(1, std::min(2048, (rows + kGatherRows - 1) / kGatherRows));
-    // pieces per thread: Q rows up to 4096 x 16 B, K/V rows up to 1024 x 16 B
-    auto launch = [&](auto kernel) {
+    auto launch = [&](auto kernel, int rpi) {
+      const int grid = std::max(1, std::min(1024, (rows + rpi - 1) / rpi));
       hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, stream, a.B, a.S, a.kept_index,
                          a.cu_seqlens, static_cast<const u32x4*>(a.q), static_cast<const u32x4*>(a.k),
                          static_cast<const u32x4*>(a.v), static_cast<u32x4*>(a.qc),
                          static_cast<u32x4*>(a.kc), static_cast<u32x4*>(a.vc), qvec, kvvec);
     };
-    const int qpt = (qvec + 255) / 256, kpt = (kvvec + 255) / 256;
-    if (qpt <= 1 && kpt <= 1) launch(gather_rows_kernel<1, 1>);
-    else if (qpt <= 2 && kpt <= 1) launch(gather_rows_kernel<2, 1>);
-    else if (qpt <= 4 && kpt <= 1) launch(gather_rows_kernel<4, 1>);
-    else if (qpt <= 4 && kpt <= 2) launch(gather_rows_kernel<4, 2>);
-    else if (qpt <= 8 && kpt <= 2) launch(gather_rows_kernel<8, 2>);
-    else launch(gather_rows_kernel<16, 4>);
+    // 16-byte pieces per thread and row, (Q + K + V pieces) / 256: at most
+    // (4096 + 2*4096) / 256 = 48 with Hq <= LITEVLM_MAX_HEADS; about 24 loads
+    // in flight per thread
+    const int ppt = (qvec + 2 * kvvec + 255) / 256;
+    if (ppt <= 1) launch(gather_rows_kernel<1, 8>, 8);
+    else if (ppt <= 2) launch(gather_rows_kernel<2, 8>, 8);
+    else if (ppt <= 3) launch(gather_rows_kernel<3, 8>, 8);
+    else if (ppt <= 4) launch(gather_rows_kernel<4, 6>, 6);
+    else if (ppt <= 6) launch(gather_rows_kernel<6, 4>, 4);
+    else if (ppt <= 12) launch(gather_rows_kernel<12, 2>, 2);
+    else if (ppt <= 24) launch(gather_rows_kernel<24, 1>, 1);
+    else launch(gather_rows_kernel<48, 1>, 1);
   }
+
   return hipGetLastError();
 }
 

@@ -43,6 +43,7 @@ def test_header_constants_match_binding():
     assert int(re.search(r"LITEVLM_MAX_VIEWS (\d+)", text).group(1)) == _abi.MAX_VIEWS
     assert int(re.search(r"LITEVLM_MAX_VISUAL (\d+)", text).group(1)) == _abi.MAX_VISUAL
     assert int(re.search(r"LITEVLM_MAX_BATCH (\d+)", text).group(1)) == _abi.MAX_BATCH
+    assert int(re.search(r"LITEVLM_MAX_HEADS (\d+)", text).group(1)) == _abi.MAX_HEADS
 
 
 # ----------------------------------------------------------------------------- patch_select
@@ -101,6 +102,7 @@ def test_token_score_topk_validation():
     assert st(dtype=7) == _abi.ERR_UNSUPPORTED
     assert st(Hkv=3) == _abi.ERR_BAD_SHAPE
     assert st(D=96) == _abi.ERR_BAD_SHAPE
+    assert st(Hq=256, Hkv=2) == _abi.ERR_BAD_SHAPE               # beyond LITEVLM_MAX_HEADS
     assert st(S=80) == _abi.ERR_BAD_SHAPE                      # T = 0
     assert st(V=20000, S=20010) == _abi.ERR_BAD_SHAPE          # beyond the top-k limit
     assert st(B=0) == _abi.ERR_BAD_SHAPE

@@ -156,6 +156,11 @@ SELECT_CASES = [
     ("fp8-small", dict(cfg=5, Tv=128, T=32)),
     ("k-zero", dict(cfg=2, Tv=16, T=8, keep_ratio=0.01)),
     ("full-keep", dict(cfg=2, Tv=64, T=16, keep_ratio=1.0, n_masked=0)),
+    # wide token rows: every gather width (16-byte pieces per thread 4, 5, 9, 32)
+    ("gather-w4", dict(cfg=2, Tv=32, T=8, Hq=40, Hkv=8, D=128)),
+    ("gather-w5", dict(cfg=2, Tv=32, T=8, Hq=48, Hkv=12, D=128)),
+    ("gather-w9", dict(cfg=2, Tv=32, T=8, Hq=48, Hkv=48, D=128)),
+    ("gather-w32-f32", dict(cfg=1, Tv=40, T=6, Hq=128, Hkv=64, D=128)),
 ]
 
 
