@@ -125,7 +125,7 @@ attn_bf16_kernel(AttnParams p) {
   constexpr int TB = BN * RB;               // bytes per tile
   constexpr int LI = TB / 1024 / NW;        // direct-copy instructions per wave per tile
   constexpr int KS = D / 16, DB = D / 32;
-  constexpr float TAU = 8.f;
+  constexpr float RS_MAX = 256.f;  // 2^TAU, TAU = 8: bound on a lane's 32 probabilities
   static_assert(LI >= 1 && TB % (1024 * NW) == 0, "tile must split into whole wave copies");
   // V swizzle: piece ^ 4*(row & 3) keeps the 4 rows x 4 pieces of a transposed
   // read distinct (D = 64 has only 8 pieces per row: piece ^ 4*(row & 1)).
@@ -282,37 +282,44 @@ attn_bf16_kernel(AttnParams p) {
             if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
           }
       }
-      float mx = max32(s);
-      {
-        const float2 pr = pair_xor32(mx);
-        mx = __builtin_elementwise_maximum(pr.x, pr.y);
-      }
-      // ---- lazy rescale
-      const bool grow = mx * c > m_run * c + TAU || (m_run == -INFINITY && mx != -INFINITY);
-      if (__any(grow)) {
-        const float m_new = grow ? fmaxf(m_run, mx) : m_run;
-        const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
+      // ---- P = exp2(s*c - m*c) under the running max m, as the B operand of
+      // O^T += V^T P^T. A lane sum above 2^TAU (so some p may exceed 2^TAU) or
+      // the first visible keys of a row send the wave through the exact path:
+      // m becomes the row max, the output so far is rescaled and P is formed
+      // again. Rows whose max grows by less than TAU keep m (lazy rescale).
+      float rsk[4];
+      bf16x8 pb[4];
+      auto form_p = [&](float mc) __attribute__((always_inline)) {
+#pragma unroll
+        for (int kk = 0; kk < 4; ++kk) {
+          float e[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][8 * (kk & 1) + i], c, -mc));
+          pb[kk] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
+                          (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
+          rsk[kk] = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
+        }
+        return (rsk[0] + rsk[1]) + (rsk[2] + rsk[3]);
+      };
+      float rs = form_p(m_run == -INFINITY ? 0.f : m_run * c);
+      const bool exact = rs > RS_MAX || (m_run == -INFINITY && rs > 0.f);
+      if (__any(exact)) {
+        float mx = max32(s);
+        {
+          const float2 pr = pair_xor32(mx);
+          mx = __builtin_elementwise_maximum(pr.x, pr.y);
+        }
+        const float m_new = fmaxf(m_run, mx);
+        const float alpha = m_new == -INFINITY ? 1.f : __builtin_amdgcn_exp2f((m_run - m_new) * c);
         l_run *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
           for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
         m_run = m_new;
+        rs = form_p(m_run == -INFINITY ? 0.f : m_run * c);
       }
-      const float mc = (m_run == -INFINITY) ? 0.f : m_run * c;
-      // ---- P = exp2(s*c - m*c) as the B operand of O^T += V^T P^T
-      float rsk[4];
-      bf16x8 pb[4];
-#pragma unroll
-      for (int kk = 0; kk < 4; ++kk) {
-        float e[8];
-#pragma unroll
-        for (int i = 0; i < 8; ++i) e[i] = __builtin_amdgcn_exp2f(fmaf(s[kk >> 1][8 * (kk & 1) + i], c, -mc));
-        pb[kk] = bf16x8{(__bf16)e[0], (__bf16)e[1], (__bf16)e[2], (__bf16)e[3],
-                        (__bf16)e[4], (__bf16)e[5], (__bf16)e[6], (__bf16)e[7]};
-        rsk[kk] = ((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7]));
-      }
-      l_run += (rsk[0] + rsk[1]) + (rsk[2] + rsk[3]);
+      l_run += rs;
       // ---- O^T += V^T P^T; V operands one k-step ahead of their MFMAs
 #pragma unroll
       for (int kk = 0; kk < 4; ++kk) {
