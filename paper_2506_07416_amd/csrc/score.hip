@@ -30,6 +30,7 @@ constexpr int kSweepWaves = 16;             // waves per sweep-1 workgroup, 32 q
 constexpr int kSweepThreads = 64 * kSweepWaves;
 constexpr int RBLK = 32 * kSweepWaves;      // query rows per sweep-1 workgroup
 constexpr int kMaxSplitTiles = 64;          // key tiles per split (one 64-bit live mask)
+constexpr int kLdsBytes = 160 * 1024;       // LDS of a workgroup (gfx950)
 // sweep 2
 constexpr int KW = 64;                      // keys per wave: 2 blocks of 32
 constexpr int kColWaves = 4;                // waves per sweep-2 workgroup
@@ -56,6 +57,30 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Workgroup barrier for LDS hand-over between the waves, with the waits
+// spelled out: this wave's LDS reads have completed (its direct copies are
+// waited for by the caller). The memory clobber keeps the compiler from moving
+// LDS accesses across it; unlike __syncthreads it carries no fence, whose
+// lowering here adds a wait for every copy in flight.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Wait until at most n (0..7; larger n waits for 7) vector-memory operations
+// of this wave are outstanding.
+__device__ __forceinline__ void wait_vmcnt_upto(int n) {
+  switch (n) {
+    case 0: wait_vmcnt<0>(); break;
+    case 1: wait_vmcnt<1>(); break;
+    case 2: wait_vmcnt<2>(); break;
+    case 3: wait_vmcnt<3>(); break;
+    case 4: wait_vmcnt<4>(); break;
+    case 5: wait_vmcnt<5>(); break;
+    case 6: wait_vmcnt<6>(); break;
+    default: wait_vmcnt<7>(); break;
+  }
+}
+
 // Flat, XCD-aware work decode. Workgroup L runs on XCD L % 8; XCD x takes the
 // contiguous column range [x*ncol/8, (x+1)*ncol/8), every column with all of
 // its splits, so the query rows of a (sample, KV group) are read into one
@@ -68,6 +93,14 @@ __device__ __forceinline__ bool decode_column(int ncol, int nsplit, int& col, in
   col = c0 + cj;
   split = j - cj * nsplit;
   return true;
+}
+
+// First key tile of split `split` of n tiles in ns splits: the first n % ns
+// splits take one tile more, so the last split (text keys, masked) is never
+// the long one.
+__device__ __forceinline__ int split_begin(int split, int n, int ns) {
+  const int base = n / ns, rem = n - base * ns;
+  return split * base + min(split, rem);
 }
 
 // ---------------------------------------------------------------- sweep-1 logit tiles
@@ -364,28 +397,39 @@ __global__ void __launch_bounds__(kSweepThreads)
 score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                       const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
   using Tile = typename RowTileOf<DT, D>::T;
-  // The workgroup's query rows pass through a 64 KB stage in rounds of QRR
-  // rows (whole rows per 1 KB direct copy, so every copy reads contiguous
-  // bytes), and each wave then reads its operand registers from the stage.
-  constexpr int QST = Tile::QSTAGE ? 65536 : 0;
-  constexpr int QRR = Tile::QSTAGE ? QST / Tile::RB : 1;
-  constexpr int NQR = Tile::QSTAGE ? (RBLK * Tile::RB + QST - 1) / QST : 0;
-  static_assert(!Tile::QSTAGE || (QST % Tile::RB == 0 && (QRR % 32) == 0), "stage rounds must hold whole waves");
+  // LDS: key-tile ring buffers j at j*TILE, then the query stage, which starts
+  // after the first two buffers: buffers 2.. overlap the stage and are first
+  // filled once every wave has read its query rows from it. The workgroup's
+  // query rows pass through the stage in rounds of QRR rows (whole rows per
+  // 1 KB direct copy, so that every copy reads contiguous bytes; one round
+  // where the rows fit), and each wave then reads its operand registers from
+  // it. The keep bytes and flag words sit after the ring, inside the stage.
+  constexpr int NPRE = Tile::NBUF < 3 ? Tile::NBUF - 1 : 2;  // key tiles in flight while the stage is in use
+  constexpr int QOFF = Tile::QSTAGE ? NPRE * Tile::TILE : Tile::NBUF * Tile::TILE;
+  constexpr int QROWS_MAX = Tile::QSTAGE ? (kLdsBytes - QOFF) / (32 * Tile::RB) * 32 : 32;
+  constexpr int QRR = Tile::QSTAGE ? (RBLK < QROWS_MAX ? RBLK : QROWS_MAX) : 1;
+  constexpr int QST = Tile::QSTAGE ? QRR * Tile::RB : 0;
+  constexpr int NQR = Tile::QSTAGE ? (RBLK + QRR - 1) / QRR : 0;
+  constexpr int FOFF = Tile::NBUF * Tile::TILE;  // keep bytes, then flag words
+  constexpr int FEND = FOFF + kMaxSplitTiles * KB + 2 * kSweepWaves * 8;
+  constexpr int LDS_BYTES = FEND > QOFF + QST ? FEND : QOFF + QST;
+  static_assert(!Tile::QSTAGE || (QRR % 32 == 0 && QST % 1024 == 0), "stage rounds must hold whole waves and copies");
+  static_assert(LDS_BYTES <= kLdsBytes, "sweep-1 LDS layout exceeds the workgroup limit");
   // One LDS object (key ring, query stage, keep bytes, flag words): with a
   // single object the compiler adds no vmcnt wait of its own before reads of
   // one buffer while direct copies into another are in flight; the explicit
   // waits and barriers order copies before reads.
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tile::NBUF * Tile::TILE + QST + kMaxSplitTiles * KB + 2 * kSweepWaves * 8];
-  uint8_t* qstage = lds + Tile::NBUF * Tile::TILE;
-  uint8_t* keepl = qstage + QST;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[LDS_BYTES];
+  uint8_t* qstage = lds + QOFF;
+  uint8_t* keepl = lds + FOFF;
   uint64_t* mw = reinterpret_cast<uint64_t*>(keepl + kMaxSplitTiles * KB);
 
   int col, split;
   if (!decode_column(d.B * d.Hkv * d.n_rb, d.ns1, col, split)) return;
   const int bg = col / d.n_rb, rb = col - bg * d.n_rb;
   const int b = bg / d.Hkv, g = bg - b * d.Hkv;
-  const int tile0 = (int)((long long)split * d.n_kt / d.ns1);
-  const int ntl = (int)((long long)(split + 1) * d.n_kt / d.ns1) - tile0;
+  const int tile0 = split_begin(split, d.n_kt, d.ns1);
+  const int ntl = split_begin(split + 1, d.n_kt, d.ns1) - tile0;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int lq = lane & 31, hl = lane >> 5;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
@@ -409,23 +453,22 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   };
   const int my_round = (32 * w) / QRR, srow = 32 * w + lq - my_round * QRR;
 
-  // keep bytes, the first query round and the first NBUF-1 key tiles, all in flight together
-  uint8_t kf[kFlagsPer];
-  load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
-  if (Tile::QSTAGE) q_round(0);
+  // The first key tiles, the first query round and the keep bytes, all in
+  // flight together: the key tiles (not shared with other workgroups, so
+  // mostly from HBM) go first, their latency hidden behind the query copies;
+  // the keep bytes go last, since their first use waits for them (and, loads
+  // completing in order, for everything before them).
   Tile tile;
   KeyPipe<Tile> pipe(lds, k + ((size_t)b * d.S * d.Hkv + g) * Tile::RB, (size_t)d.Hkv * Tile::RB, tile0, ntl,
                      d.S, w, lane);
 #pragma unroll
-  for (int t = 0; t < Tile::NBUF - 1; ++t) pipe.issue(t);
+  for (int t = 0; t < (Tile::QSTAGE ? NPRE : Tile::NBUF - 1); ++t) pipe.issue(t);
+  if (Tile::QSTAGE) q_round(0);
+  asm volatile("" ::: "memory");  // keep the copies ahead of the keep-byte loads
+  uint8_t kf[kFlagsPer];
+  load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
   if (Tile::QSTAGE) {
-    // round 0 has landed once at most the key copies issued after it remain
-    switch (min(Tile::NBUF - 1, ntl) * pipe.cpw) {
-      case 0: wait_vmcnt<0>(); break;
-      case 1: wait_vmcnt<1>(); break;
-      case 2: wait_vmcnt<2>(); break;
-      default: wait_vmcnt<3>(); break;
-    }
+    wait_vmcnt<0>();  // round 0, the first key tiles and the keep bytes have landed
     __syncthreads();
     if (wave_active && my_round == 0) tile.init_lds(qstage, srow, lane);
     for (int round = 1; round < NQR; ++round) {
@@ -435,6 +478,9 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
       __syncthreads();
       if (wave_active && my_round == round) tile.init_lds(qstage, srow, lane);
     }
+    __syncthreads();  // every read of the stage is done: buffers 2.. may be filled
+#pragma unroll
+    for (int t = NPRE; t < Tile::NBUF - 1; ++t) pipe.issue(t);
   }
   pipe.wait_for(0);
   __syncthreads();  // tile 0 and the keep bytes have landed
@@ -451,13 +497,18 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
     if (!((plain >> t) & 1ull)) {
       // visible: kept visual keys, and text keys V_full + t' with t' <= the row's token
       const int key0 = (tile0 + t) * KB;
-      const uint32_t kept = lane_kept_bits(keepl + t * KB, lane);
-      const int nv = keys_upto(d.V_full - 1 - key0 - 4 * hl);   // keys < V_full
       const int ns = keys_upto(d.S - 1 - key0 - 4 * hl);        // keys < S
       const int n1 = min(keys_upto(d.V_full + t_row - key0 - 4 * hl), ns);
       const uint32_t below_n1 = n1 >= 32 ? 0xFFFFFFFFu : ((1u << n1) - 1u);
-      const uint32_t below_nv = nv >= 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
-      const uint32_t vis = kept | (below_n1 & ~below_nv);
+      uint32_t vis;
+      if (key0 >= d.V_full) {
+        vis = below_n1;  // text keys only: the causal limit alone
+      } else {
+        const uint32_t kept = lane_kept_bits(keepl + t * KB, lane);
+        const int nv = keys_upto(d.V_full - 1 - key0 - 4 * hl);   // keys < V_full
+        const uint32_t below_nv = nv >= 32 ? 0xFFFFFFFFu : ((1u << nv) - 1u);
+        vis = kept | (below_n1 & ~below_nv);
+      }
 #pragma unroll
       for (int j = 0; j < 32; ++j) s[j >> 4][j & 15] = ((vis >> j) & 1u) ? s[j >> 4][j & 15] : -INFINITY;
     }
@@ -513,7 +564,7 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
 // One row per (thread % 64); the key splits go to 4 thread slices (split s to
 // slice s % 4), and the slices are combined in slice order. With at most
 // 4*kMergeMax splits a slice holds its values in registers (one pass over
-// memory), otherwise it reads them twice. rowstat = (max in log2 units, 1/sum).
+// memory), otherwise it reads them twice. rowstat = (-max in log2 units, 1/sum).
 
 constexpr int kMergeMax = 16;
 
@@ -557,30 +608,34 @@ score_rowmerge_kernel(int rows_total, int R, int nsplit, const float2* __restric
   __syncthreads();
   if (slice == 0 && ok) {
     const float zt = ((red[1][0][slot] + red[1][1][slot]) + red[1][2][slot]) + red[1][3][slot];
-    rowstat[idx] = make_float2(m, 1.0f / zt);
+    rowstat[idx] = make_float2(-m, 1.0f / zt);
   }
 }
 
 // ---------------------------------------------------------------- sweep-2 logit tiles
 // A sweep-2 tile policy holds one wave's 64 keys of one KV head in registers
-// (the A operand of S^T = K Q^T) and forms, for the 32 query rows of a chunk
-// staged in LDS, s[nb][r] = k(32*nb + acc_row(r)) . q(lane % 32) in fp32.
-// ro[] are the lane's byte offsets of its B-operand pieces within a chunk.
+// (the B operand of S = Q K^T) and forms, for the 32 query rows of a chunk
+// staged in LDS, s[nb][r] = q(acc_row(r)) . k(32*nb + lane % 32) in fp32: a
+// lane owns one key column of each 32-key block. ro[] are the lane's byte
+// offsets of its A-operand pieces within a chunk.
 
 template <int D>
 struct ColTileBf16 {
   static constexpr int RB = D * 2;        // bytes per row
   static constexpr int NP = RB / 16;      // 16-byte pieces per row
   static constexpr int KS = D / 16;       // k-steps of v_mfma_f32_32x32x16_bf16
+  static_assert(NP == 2 * KS && (NP & (NP - 1)) == 0, "piece index 2*ks + hl must fit the XOR swizzle");
   bf16x8 kreg[2][KS];
-  uint32_t ro[KS];
+  // LDS offset of the lane's k-step 0 piece within a chunk (row lane % 32); the
+  // piece of k-step ks is at rbase ^ (32*ks) (piece 2*ks + hl = (2*ks) ^ hl,
+  // and the swizzle is an XOR below bit 4 of the row offset)
+  uint32_t rbase;
   // LDS piece swizzle of Q rows: each 16-lane group reads 16 rows x 1 piece
   __device__ __forceinline__ static int qswz(int r) { return r & (NP - 1); }
 
   __device__ __forceinline__ void init(int lane) {
     const int lq = lane & 31, hl = lane >> 5;
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) ro[ks] = lq * RB + ((2 * ks + hl) ^ qswz(lq)) * 16;
+    rbase = lq * RB + (hl ^ qswz(lq)) * 16;
   }
 
   __device__ __forceinline__ void load_keys(const uint8_t* kbase, size_t kstride, int nvalid, int lane) {
@@ -600,12 +655,15 @@ struct ColTileBf16 {
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+    // re-derived per chunk, so that the compiler does not keep all KS offsets live
+    uint32_t rb = rbase;
+    asm volatile("" : "+v"(rb));
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 qb = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + ro[ks]));
+      const bf16x8 qb = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(buf + (rb ^ (32u * ks))));
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
-        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kreg[nb][ks], qb, s[nb], 0, 0, 0);
+        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(qb, kreg[nb][ks], s[nb], 0, 0, 0);
     }
   }
 };
@@ -656,15 +714,15 @@ struct ColTileFp8 {
 #pragma unroll
       for (int nb = 0; nb < 2; ++nb)
         // format 0 = E4M3 for both operands; zero scale operands select the unscaled instruction
-        s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(kreg[nb][ks], qb, s[nb], 0, 0, 0, 0, 0, 0);
+        s[nb] = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(qb, kreg[nb][ks], s[nb], 0, 0, 0, 0, 0, 0);
     }
   }
 };
 
 template <int D>
 struct ColTileF32 {
-  // Plain fp32 FMAs; fp32 inputs are only used at small sizes. The lane's 32
-  // accumulator keys are read from global memory, its query row from LDS.
+  // Plain fp32 FMAs; fp32 inputs are only used at small sizes. The lane's two
+  // keys are read from global memory, its 16 accumulator rows from LDS.
   static constexpr int RB = D * 4;
   static constexpr int NP = RB / 16;
   const uint8_t* kbase;
@@ -681,18 +739,18 @@ struct ColTileF32 {
 
   __device__ __forceinline__ void logits(const uint8_t* buf, int lane, f32x16 s[2]) const {
     const int lq = lane & 31, hl = lane >> 5;
-    const float* qf = reinterpret_cast<const float*>(buf + lq * RB);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < 2; ++nb) {
+      const int key = nb * 32 + lq;
+      const float* kr = reinterpret_cast<const float*>(kbase + min(key, max(nvalid - 1, 0)) * kstride);
       for (int r = 0; r < 16; ++r) {
-        const int key = nb * 32 + acc_row(r, hl);
+        const float* qf = reinterpret_cast<const float*>(buf + acc_row(r, hl) * RB);
         float acc = 0.f;
-        if (key < nvalid) {
-          const float* kr = reinterpret_cast<const float*>(kbase + key * kstride);
+        if (key < nvalid)
           for (int dd = 0; dd < D; ++dd) acc = fmaf(qf[dd], kr[dd], acc);
-        }
         s[nb][r] = acc;
       }
+    }
   }
 };
 
@@ -702,34 +760,46 @@ template <int D> struct ColTileOf<LITEVLM_BF16, D> { using T = ColTileBf16<D>; }
 template <int D> struct ColTileOf<LITEVLM_FP8_E4M3, D> { using T = ColTileFp8<D>; };
 template <int D> struct ColTileOf<LITEVLM_F32, D> { using T = ColTileF32<D>; };
 
-// Text query rows of a workgroup pass through two chunk buffers in LDS,
+// Text query rows of a workgroup pass through three chunk buffers in LDS,
 // filled with direct global -> LDS copies (16-byte pieces, XOR-swizzled per
 // row) two chunks ahead of use. Row r of KV group g is query head g*G + r%G
 // of text token r/G; each lane tracks (token, head) of its copies and steps
 // them by the row distance between the workgroup's chunks. Rows past R repeat
-// a valid row; callers ignore them.
+// a valid row; callers ignore them. Behind each chunk's rows sit their 32
+// (-max, 1/sum) statistics (256 bytes, one 4-byte copy per lane of wave 0).
 template <class Tile>
 struct QRing {
   static constexpr int RB = Tile::RB;
   static constexpr int NP = Tile::NP;
-  static constexpr int CB = CH * RB;                            // bytes per chunk
+  static constexpr int CB = CH * RB;                            // bytes of a chunk's rows
+  static constexpr int SB = CH * 8;                             // bytes of a chunk's statistics
+  static constexpr int BUFB = CB + SB;                          // bytes per chunk buffer
   static constexpr int IPC = CB / 1024;                         // wave copies per chunk
   static constexpr int CPW = (IPC + kColWaves - 1) / kColWaves;
-  static constexpr int BYTES = 2 * CB;
+  static constexpr int NBUF = 3;
+  static constexpr int BYTES = NBUF * BUFB;
   static_assert(CB % 1024 == 0, "a chunk must split into whole wave copies");
   static_assert(IPC % kColWaves == 0 || IPC < kColWaves, "copies must split evenly over waves");
+  static_assert(SB == 64 * 4, "one 4-byte copy per lane carries a chunk's statistics");
 
   const uint8_t* qbase;  // row (text token 0, head g*G) of this sample and group
-  int G, Hq, T, dt, dh;
+  const float* sbase;    // statistics of row 0 of this sample and group
+  int G, Hq, T, R, dt, dh;
+  int srow;              // first row of the next chunk
+  int cstep;
   int t[CPW], hh[CPW];
   uint32_t src[CPW];     // byte offset of the lane's piece within its row
 
-  __device__ __forceinline__ void init(const uint8_t* q, int b, int g, const ScoreDims& d, int w, int lane,
-                                       int row0, int cstep) {
+  __device__ __forceinline__ void init(const uint8_t* q, const float2* rowstat, int b, int g, const ScoreDims& d,
+                                       int w, int lane, int row0, int cstep_) {
     qbase = q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * RB;
+    sbase = reinterpret_cast<const float*>(rowstat + ((size_t)b * d.Hkv + g) * d.R);
     G = d.G;
     Hq = d.Hq;
     T = d.T;
+    R = d.R;
+    cstep = cstep_;
+    srow = row0;
     dt = cstep / d.G;
     dh = cstep - dt * d.G;
 #pragma unroll
@@ -743,8 +813,23 @@ struct QRing {
     }
   }
 
+  // number of copies that issue() makes for wave w
+  __device__ __forceinline__ static int copies(int w) {
+    int n = w == 0 ? 1 : 0;
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) n += (w + kColWaves * j < IPC) ? 1 : 0;
+    return n;
+  }
+
   // copies of the current chunk into buf, then step to the workgroup's next chunk
-  __device__ __forceinline__ void issue(uint8_t* buf, int w) {
+  __device__ __forceinline__ void issue(uint8_t* buf, int w, int lane) {
+    if (w == 0) {
+      // float (lane % 2) of row srow + lane/2, clamped to row R-1 (rows past R are masked by the reader)
+      const int r = min(srow + (lane >> 1), R - 1);
+      __builtin_amdgcn_global_load_lds((const void*)(sbase + 2 * (size_t)r + (lane & 1)),
+                                       (__attribute__((address_space(3))) void*)(buf + CB), 4, 0, 0);
+    }
+    srow += cstep;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
       const int sub = w + kColWaves * j;
@@ -764,13 +849,6 @@ struct QRing {
   }
 };
 
-// True on every lane when all 64 keys of the wave are kept visual keys.
-__device__ __forceinline__ bool wave_all_visible(const uint8_t* keep_row, int key0, int V_full, int S, int lane) {
-  const int key = key0 + lane;
-  const uint8_t f = keep_row ? keep_row[min(key, S - 1)] : 1;
-  return __ballot(key < V_full && f) == ~0ull;
-}
-
 // Workgroup-wide OR through four per-wave words of the kernel's own LDS
 // array (the runtime's block reduction would add an LDS object of its own).
 __device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
@@ -782,31 +860,11 @@ __device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
   return r;
 }
 
-// Bit j (j = 16*nb + r) of the lane's 32 accumulator keys key0 + 32*nb +
-// acc_row(r, lane/32) set where key < limit and kept. Keys ascend with j.
-__device__ __forceinline__ uint32_t lane_key_bits(const uint8_t* keep_row, int key0, int limit, int S,
-                                                  int lane) {
-  const int hl = lane >> 5;
-  uint32_t m = 0;
-  if (keep_row) {
-    uint8_t f[32];
-#pragma unroll
-    for (int j = 0; j < 32; ++j) f[j] = keep_row[min(key0 + (j >> 4) * 32 + acc_row(j & 15, hl), S - 1)];
-#pragma unroll
-    for (int j = 0; j < 32; ++j)
-      m |= (uint32_t)((key0 + (j >> 4) * 32 + acc_row(j & 15, hl) < limit) & (f[j] != 0)) << j;
-  } else {
-#pragma unroll
-    for (int j = 0; j < 32; ++j) m |= (uint32_t)(key0 + (j >> 4) * 32 + acc_row(j & 15, hl) < limit) << j;
-  }
-  return m;
-}
-
 // ---------------------------------------------------------------- sweep 2
 // Flat grid over columns (b, g, visual key tile vt of KT keys) x rs2 row splits. Each
-// wave owns 64 keys and accumulates exp2(logit - m)/Z over the workgroup's
-// rows per lane, then sums the 32 rows of a lane half by DPP and a permlane
-// swap into colpart[b][g][split][V_full].
+// wave owns 64 keys; a lane accumulates exp2(logit - m)/Z of its key column
+// over the 16 accumulator rows it holds of each chunk, so only the two lane
+// halves (disjoint rows) are summed at the end, into colpart[b][g][split][V_full].
 
 template <int DT, int D>
 __global__ void __launch_bounds__(256, 3)
@@ -815,8 +873,8 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
                      float* __restrict__ colpart) {
   using Tile = typename ColTileOf<DT, D>::T;
   using Ring = QRing<Tile>;
-  // one LDS object (see sweep 1): the two query-row chunk buffers
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES];
+  // one LDS object (see sweep 1): the chunk buffers, then four flag words
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES + 16];
 
   int col, rs;
   if (!decode_column(d.B * d.Hkv * d.n_vt, d.rs2, col, rs)) return;
@@ -825,7 +883,7 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   const uint8_t* q = static_cast<const uint8_t*>(qv);
   const uint8_t* k = static_cast<const uint8_t*>(kv);
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int lq = lane & 31, hl = lane >> 5;
+  const int hl = lane >> 5;
   const int key0 = vt * KT + w * KW;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
   float* out = colpart + (((size_t)b * d.Hkv + g) * d.rs2 + rs) * d.V_full;
@@ -833,81 +891,91 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   const int cstep = d.rs2 * CH;
   const int row0 = rs * CH;
 
+  // The keys, the first two chunks and the keep byte of the thread's key are
+  // all in flight together; the keep bytes go last (their first use waits
+  // for them and, loads completing in order, for everything before them).
+  Ring ring;
+  ring.init(q, rowstat, b, g, d, w, lane, row0, cstep);
+  Tile tile;
+  tile.init(lane);
+  tile.load_keys(k + (((size_t)b * d.S + min(key0, d.V_full - 1)) * d.Hkv + g) * Tile::RB,
+                 (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.V_full - key0)), lane);
+  ring.issue(lds, w, lane);
+  if (nch > 1) ring.issue(lds + Ring::BUFB, w, lane);
+  asm volatile("" ::: "memory");  // keep the copies ahead of the keep-byte load
   const int tkey = vt * KT + tid;
-  const bool tkept = tkey < d.V_full && (keep_row == nullptr || keep_row[tkey]);
-  if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds))) {
-    // no kept key in the tile: its column mass is 0
-    if (tkey < d.V_full) out[tkey] = 0.f;
-  } else {
-    const float2* rstat = rowstat + ((size_t)b * d.Hkv + g) * d.R;
-    // (m, 1/Z) of the lane's row of chunk i; rows past R get m = +inf so that
-    // their terms vanish
-    auto row_stat = [&](int i) {
-      const int r = row0 + i * cstep + lq;
-      const float2 v = rstat[min(r, d.R - 1)];
-      return r < d.R ? v : make_float2(INFINITY, 0.f);
-    };
-    float2 st[2];
-    st[0] = row_stat(0);
-    st[1] = make_float2(INFINITY, 0.f);
-
-    Ring ring;
-    ring.init(q, b, g, d, w, lane, row0, cstep);
-    ring.issue(lds, w);
-    Tile tile;
-    tile.init(lane);
-    tile.load_keys(k + (((size_t)b * d.S + min(key0, d.V_full - 1)) * d.Hkv + g) * Tile::RB,
-                   (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.V_full - key0)), lane);
-    if (nch > 1) ring.issue(lds + Ring::CB, w);
-    const float c = d.scale_log2;
-
-    f32x16 acc[2];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nb][r] = 0.f;
+  const bool tkept = tkey < d.V_full && (keep_row == nullptr || keep_row[min(tkey, d.V_full - 1)]);
+  // the flag words of block_any sit past the chunk buffers, which are being filled
+  if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds + Ring::BYTES))) {
+    // no kept key in the tile: its column mass is 0 (the copies into LDS
+    // land before the workgroup ends)
     wait_vmcnt<0>();
-    __syncthreads();
+    if (tkey < d.V_full) out[tkey] = 0.f;
+    return;
+  }
+  const float c = d.scale_log2;
+  const int cpw = __builtin_amdgcn_readfirstlane(Ring::copies(w));  // wave-uniform: scalar branches
 
-    auto body = [&](auto bufc, int i) {
-      constexpr int BUF = decltype(bufc)::value;
-      f32x16 s[2];
-      tile.logits(lds + BUF * Ring::CB, lane, s);
-      wait_vmcnt<0>();
-      __syncthreads();
-      // the row statistics load goes first: loads complete in order
-      if (i + 1 < nch) st[BUF ^ 1] = row_stat(i + 1);
-      if (i + 2 < nch) ring.issue(lds + BUF * Ring::CB, w);
-      const float ms = -st[BUF].x, iz = st[BUF].y;
+  // four partial sums per key column (accumulator rows r with r % 4 = j)
+  float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+
+  // Chunk i sits in buffer i % 3. Step i waits for its copies (those of chunk
+  // i+1 may stay in flight; loads complete in order), and its barrier also
+  // marks the end of every read of chunk i-1, whose buffer then takes chunk i+2.
+  auto body = [&](auto bufc, int i) {
+    constexpr int BUF = decltype(bufc)::value;
+    const uint8_t* buf = lds + BUF * Ring::BUFB;
+    wait_vmcnt_upto(i + 1 < nch ? cpw : 0);
+    lds_barrier();
+    if (i + 2 < nch) ring.issue(lds + ((BUF + 2) % Ring::NBUF) * Ring::BUFB, w, lane);
+    f32x16 s[2];
+    tile.logits(buf, lane, s);
+    // (-max, 1/sum) of the lane's accumulator rows 8*j + 4*hl + 0..3
+    f32x4 st[8];
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[nb][r] = fmaf(__builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms)), iz, acc[nb][r]);
-    };
-    for (int i = 0; i < nch; i += 2) {
-      body(std::integral_constant<int, 0>{}, i);
-      if (i + 1 < nch) body(std::integral_constant<int, 1>{}, i + 1);
+    for (int j = 0; j < 4; ++j) {
+      const f32x4* sp = reinterpret_cast<const f32x4*>(buf + Ring::CB + (8 * j + 4 * hl) * 8);
+      st[2 * j] = sp[0];
+      st[2 * j + 1] = sp[1];
     }
-    // sum over the 32 rows of each lane half (lanes sharing lane/32), fixed tree
+    const int valid = d.R - (row0 + i * cstep);  // rows of this chunk below R
+    if (valid < CH) {
+      // rows past R: exp2(-inf) = 0 and a zero weight
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[nb][r] = sum_xor16(row16_sum(acc[nb][r]));
-    const uint32_t vis = wave_all_visible(keep_row, key0, d.V_full, d.S, lane)
-                             ? 0xFFFFFFFFu
-                             : lane_key_bits(keep_row, key0, d.V_full, d.S, lane);
-    if (lq == 0) {
-#pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int key = key0 + nb * 32 + acc_row(r, hl);
-          // dropped keys were summed over too; their column is forced to 0
-          if (key < d.V_full) out[key] = ((vis >> (nb * 16 + r)) & 1u) ? acc[nb][r] : 0.f;
+      for (int r = 0; r < 16; ++r)
+        if (acc_row(r, hl) >= valid) {
+          if (r & 1) { st[r >> 1].z = -INFINITY; st[r >> 1].w = 0.f; }
+          else { st[r >> 1].x = -INFINITY; st[r >> 1].y = 0.f; }
         }
     }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float ms = (r & 1) ? st[r >> 1].z : st[r >> 1].x;
+        const float iz = (r & 1) ? st[r >> 1].w : st[r >> 1].y;
+        acc[nb][r & 3] = fmaf(__builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms)), iz, acc[nb][r & 3]);
+      }
+  };
+  for (int i = 0; i < nch; i += 3) {
+    body(std::integral_constant<int, 0>{}, i);
+    if (i + 1 < nch) body(std::integral_constant<int, 1>{}, i + 1);
+    if (i + 2 < nch) body(std::integral_constant<int, 2>{}, i + 2);
   }
-
+  // the lane's key column over its rows, then the other lane half's rows:
+  // lane L ends with key key0 + L
+  float tot[2];
+#pragma unroll
+  for (int nb = 0; nb < 2; ++nb) tot[nb] = (acc[nb][0] + acc[nb][1]) + (acc[nb][2] + acc[nb][3]);
+  const float give = hl ? tot[0] : tot[1];
+  const float got = __shfl_xor(give, 32);
+  const float colmass = (hl ? tot[1] : tot[0]) + got;
+  const int key = key0 + lane;
+  if (key < d.V_full) {
+    // dropped keys were summed over too; their column is forced to 0
+    const bool kept = keep_row == nullptr || keep_row[key];
+    out[key] = kept ? colmass : 0.f;
+  }
 }
 
 // ---------------------------------------------------------------- column sum
