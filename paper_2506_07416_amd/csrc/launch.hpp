@@ -19,13 +19,12 @@ hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const
                                uint8_t* token_keep, int32_t* n_visual_kept, hipStream_t stream);
 
 // Workspace of the scoring step, carved from one caller buffer:
-//   rowpart  float2 [B][Hkv][ns1][R]      per-key-split (max, sum) of each text row
-//   rowstat  float2 [B][Hkv][R]           merged (max, 1/sum) per text row
-//   colpart  float  [B][Hkv][rs2][V_full] column mass per KV group and row split
-// with R = (Hq/Hkv)*T rows per KV group; ns1 (key splits of sweep 1) and rs2
-// (row splits of sweep 2) are functions of the shape.
+//   rowpart  float2 [B][Hkv][ns1][R]  per-key-split (max, sum) of each text row
+//   acc      u64    [B][V_full]       fixed-point column sums of sweep 2
+// with R = (Hq/Hkv)*T rows per KV group; ns1 (key splits of sweep 1) is a
+// function of the shape.
 struct ScoreWorkspace {
-  size_t rowpart_off, rowstat_off, colpart_off, total;
+  size_t rowpart_off, acc_off, total;
 };
 ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv);
 

@@ -8,15 +8,18 @@
 // keys V_full+t' with t' <= t. Exact column mass needs each row's softmax
 // normaliser first, so the work is two sweeps over K:
 //   sweep 1  per (key split, row): max m and sum Z of exp2(logit) over the split
-//   merge    per row: m = max over splits, Z = sum Z_split * exp2(m_split - m)
-//   sweep 2  per visual key: sum over rows of exp2(logit - m) / Z
+//   sweep 2  per row (merged at the start of each workgroup): m = max over
+//            splits, Z = sum Z_split * exp2(m_split - m); then per visual key:
+//            sum over rows of exp2(logit - m) / Z
 // Both sweeps form logits on 32x32 MFMAs. Sweep 1 keeps 32 query rows per wave
 // in registers and streams key tiles through LDS (a lane owns one query row of
 // the transposed block, so its row statistics stay in the lane). Sweep 2 keeps
 // 64 keys per wave in registers and streams query rows through LDS (a lane owns
 // one key column, so its column mass accumulates in the lane). Every reduction
-// runs in a fixed order, so results are deterministic.
+// runs in a fixed order, and the column partials of the workgroups are added
+// as fixed-point integers, so results are deterministic.
 #include <algorithm>
+#include <cmath>
 #include <type_traits>
 
 #include "common.hpp"
@@ -50,6 +53,7 @@ struct ScoreDims {
   int B, S, V_full, T, Hq, Hkv, G, R;
   int n_rb, n_kt, ns1, n_vt, nchunks, rs2;
   float scale_log2;
+  float fx;  // fixed-point scale of the column sums (a power of two)
 };
 
 template <int N>
@@ -395,7 +399,8 @@ __device__ __forceinline__ int keys_upto(int L) {
 template <int DT, int D>
 __global__ void __launch_bounds__(kSweepThreads)
 score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
-                      const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart) {
+                      const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart,
+                      unsigned long long* __restrict__ acc) {
   using Tile = typename RowTileOf<DT, D>::T;
   // LDS: key-tile ring buffers j at j*TILE, then the query stage, which starts
   // after the first two buffers: buffers 2.. overlap the stage and are first
@@ -423,6 +428,10 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   uint8_t* qstage = lds + QOFF;
   uint8_t* keepl = lds + FOFF;
   uint64_t* mw = reinterpret_cast<uint64_t*>(keepl + kMaxSplitTiles * KB);
+
+  // the column sums of sweep 2 start from zero (this grid runs before it)
+  for (int i = blockIdx.x * kSweepThreads + threadIdx.x; i < d.B * d.V_full; i += gridDim.x * kSweepThreads)
+    acc[i] = 0ull;
 
   int col, split;
   if (!decode_column(d.B * d.Hkv * d.n_rb, d.ns1, col, split)) return;
@@ -558,58 +567,6 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   if (hl == 0 && row < d.R)
     rowpart[(((size_t)b * d.Hkv + g) * d.ns1 + split) * d.R + row] =
         make_float2(m_run == -INFINITY ? -INFINITY : m_run * c, z);
-}
-
-// ---------------------------------------------------------------- merge
-// One row per (thread % 64); the key splits go to 4 thread slices (split s to
-// slice s % 4), and the slices are combined in slice order. With at most
-// 4*kMergeMax splits a slice holds its values in registers (one pass over
-// memory), otherwise it reads them twice. rowstat = (-max in log2 units, 1/sum).
-
-constexpr int kMergeMax = 16;
-
-template <bool REG>
-__global__ void __launch_bounds__(256)
-score_rowmerge_kernel(int rows_total, int R, int nsplit, const float2* __restrict__ rowpart,
-                      float2* __restrict__ rowstat) {
-  __shared__ float red[2][4][64];
-  const int tid = threadIdx.x, slot = tid & 63, slice = tid >> 6;
-  const int idx = blockIdx.x * 64 + slot;
-  const bool ok = idx < rows_total;
-  const int bg = ok ? idx / R : 0, r = ok ? idx - bg * R : 0;
-  const float2* p = rowpart + (size_t)bg * nsplit * R + r;
-  const int mine = ok ? (nsplit - slice + 3) / 4 : 0;  // splits slice, slice + 4, ...
-  float2 v[REG ? kMergeMax : 1];
-  float m = -INFINITY;
-  if (REG) {
-#pragma unroll
-    for (int i = 0; i < kMergeMax; ++i)
-      v[i] = i < mine ? p[(size_t)(slice + 4 * i) * R] : make_float2(-INFINITY, 0.f);
-#pragma unroll
-    for (int i = 0; i < kMergeMax; ++i) m = fmaxf(m, v[i].x);
-  } else {
-    for (int i = 0; i < mine; ++i) m = fmaxf(m, p[(size_t)(slice + 4 * i) * R].x);
-  }
-  red[0][slice][slot] = m;
-  __syncthreads();
-  m = fmaxf(fmaxf(red[0][0][slot], red[0][1][slot]), fmaxf(red[0][2][slot], red[0][3][slot]));
-  float z = 0.f;
-  if (REG) {
-#pragma unroll
-    for (int i = 0; i < kMergeMax; ++i)
-      if (v[i].x != -INFINITY) z += v[i].y * exp2f(v[i].x - m);
-  } else {
-    for (int i = 0; i < mine; ++i) {
-      const float2 u = p[(size_t)(slice + 4 * i) * R];
-      if (u.x != -INFINITY) z += u.y * exp2f(u.x - m);
-    }
-  }
-  red[1][slice][slot] = z;
-  __syncthreads();
-  if (slice == 0 && ok) {
-    const float zt = ((red[1][0][slot] + red[1][1][slot]) + red[1][2][slot]) + red[1][3][slot];
-    rowstat[idx] = make_float2(-m, 1.0f / zt);
-  }
 }
 
 // ---------------------------------------------------------------- sweep-2 logit tiles
@@ -765,41 +722,30 @@ template <int D> struct ColTileOf<LITEVLM_F32, D> { using T = ColTileF32<D>; };
 // row) two chunks ahead of use. Row r of KV group g is query head g*G + r%G
 // of text token r/G; each lane tracks (token, head) of its copies and steps
 // them by the row distance between the workgroup's chunks. Rows past R repeat
-// a valid row; callers ignore them. Behind each chunk's rows sit their 32
-// (-max, 1/sum) statistics (256 bytes, one 4-byte copy per lane of wave 0).
+// a valid row; their statistics make their terms vanish.
 template <class Tile>
 struct QRing {
   static constexpr int RB = Tile::RB;
   static constexpr int NP = Tile::NP;
-  static constexpr int CB = CH * RB;                            // bytes of a chunk's rows
-  static constexpr int SB = CH * 8;                             // bytes of a chunk's statistics
-  static constexpr int BUFB = CB + SB;                          // bytes per chunk buffer
+  static constexpr int CB = CH * RB;                            // bytes per chunk
   static constexpr int IPC = CB / 1024;                         // wave copies per chunk
   static constexpr int CPW = (IPC + kColWaves - 1) / kColWaves;
   static constexpr int NBUF = 3;
-  static constexpr int BYTES = NBUF * BUFB;
+  static constexpr int BYTES = NBUF * CB;
   static_assert(CB % 1024 == 0, "a chunk must split into whole wave copies");
   static_assert(IPC % kColWaves == 0 || IPC < kColWaves, "copies must split evenly over waves");
-  static_assert(SB == 64 * 4, "one 4-byte copy per lane carries a chunk's statistics");
 
   const uint8_t* qbase;  // row (text token 0, head g*G) of this sample and group
-  const float* sbase;    // statistics of row 0 of this sample and group
-  int G, Hq, T, R, dt, dh;
-  int srow;              // first row of the next chunk
-  int cstep;
+  int G, Hq, T, dt, dh;
   int t[CPW], hh[CPW];
   uint32_t src[CPW];     // byte offset of the lane's piece within its row
 
-  __device__ __forceinline__ void init(const uint8_t* q, const float2* rowstat, int b, int g, const ScoreDims& d,
-                                       int w, int lane, int row0, int cstep_) {
+  __device__ __forceinline__ void init(const uint8_t* q, int b, int g, const ScoreDims& d, int w, int lane,
+                                       int row0, int cstep) {
     qbase = q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * RB;
-    sbase = reinterpret_cast<const float*>(rowstat + ((size_t)b * d.Hkv + g) * d.R);
     G = d.G;
     Hq = d.Hq;
     T = d.T;
-    R = d.R;
-    cstep = cstep_;
-    srow = row0;
     dt = cstep / d.G;
     dh = cstep - dt * d.G;
 #pragma unroll
@@ -815,21 +761,14 @@ struct QRing {
 
   // number of copies that issue() makes for wave w
   __device__ __forceinline__ static int copies(int w) {
-    int n = w == 0 ? 1 : 0;
+    int n = 0;
 #pragma unroll
     for (int j = 0; j < CPW; ++j) n += (w + kColWaves * j < IPC) ? 1 : 0;
     return n;
   }
 
   // copies of the current chunk into buf, then step to the workgroup's next chunk
-  __device__ __forceinline__ void issue(uint8_t* buf, int w, int lane) {
-    if (w == 0) {
-      // float (lane % 2) of row srow + lane/2, clamped to row R-1 (rows past R are masked by the reader)
-      const int r = min(srow + (lane >> 1), R - 1);
-      __builtin_amdgcn_global_load_lds((const void*)(sbase + 2 * (size_t)r + (lane & 1)),
-                                       (__attribute__((address_space(3))) void*)(buf + CB), 4, 0, 0);
-    }
-    srow += cstep;
+  __device__ __forceinline__ void issue(uint8_t* buf, int w) {
 #pragma unroll
     for (int j = 0; j < CPW; ++j) {
       const int sub = w + kColWaves * j;
@@ -861,20 +800,31 @@ __device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
 }
 
 // ---------------------------------------------------------------- sweep 2
-// Flat grid over columns (b, g, visual key tile vt of KT keys) x rs2 row splits. Each
-// wave owns 64 keys; a lane accumulates exp2(logit - m)/Z of its key column
-// over the 16 accumulator rows it holds of each chunk, so only the two lane
-// halves (disjoint rows) are summed at the end, into colpart[b][g][split][V_full].
+// Flat grid over columns (b, g, visual key tile vt of KT keys) x rs2 row splits.
+// A workgroup first merges the sweep-1 partials of its rows into per-row
+// (-max, 1/sum) in LDS: m = max over splits, Z = sum Z_split * exp2(m_split -
+// m). Each wave owns 64 keys; a lane accumulates exp2(logit - m)/Z of its key
+// column over the 16 accumulator rows it holds of each chunk, so only the two
+// lane halves (disjoint rows) are summed at the end. The workgroup's column
+// partials go into acc[b][key] as fixed-point integers (value * fx, rounded
+// to nearest): integer addition is associative, so the sums do not depend on
+// the order in which the workgroups add them.
+
+constexpr int kMaxChunksPerSplit = 32;  // row chunks of one sweep-2 workgroup (table of 8 KB)
 
 template <int DT, int D>
-__global__ void __launch_bounds__(256, 3)
+__global__ void __launch_bounds__(256, DT == LITEVLM_F32 ? 2 : 3)  // fp32 chunks: 16 KB each
 score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
-                     const uint8_t* __restrict__ token_keep, const float2* __restrict__ rowstat,
-                     float* __restrict__ colpart) {
+                     const uint8_t* __restrict__ token_keep, const float2* __restrict__ rowpart,
+                     unsigned long long* __restrict__ acc) {
   using Tile = typename ColTileOf<DT, D>::T;
   using Ring = QRing<Tile>;
-  // one LDS object (see sweep 1): the chunk buffers, then four flag words
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Ring::BYTES + 16];
+  // one LDS object (see sweep 1): the chunk buffers, the row statistics of
+  // the workgroup's rows, four flag words
+  constexpr int TAB = Ring::BYTES;
+  constexpr int FLG = TAB + kMaxChunksPerSplit * CH * 8;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[FLG + 16];
+  float2* table = reinterpret_cast<float2*>(lds + TAB);
 
   int col, rs;
   if (!decode_column(d.B * d.Hkv * d.n_vt, d.rs2, col, rs)) return;
@@ -886,67 +836,122 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   const int hl = lane >> 5;
   const int key0 = vt * KT + w * KW;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
-  float* out = colpart + (((size_t)b * d.Hkv + g) * d.rs2 + rs) * d.V_full;
   const int nch = (d.nchunks - rs + d.rs2 - 1) / d.rs2;
   const int cstep = d.rs2 * CH;
   const int row0 = rs * CH;
+  if (nch > kMaxChunksPerSplit) return;  // the host split keeps nch within the table
+
+  // Row statistics of local row lr = i*CH + j (global row row0 + i*cstep + j):
+  // P consecutive threads share a row, each taking every P-th split, and
+  // combine their (max, sum) by shuffles in fixed order. The first 2*8 splits
+  // of a thread's first row are loaded before everything else, so that they
+  // return while the keys are still in flight (loads complete in order).
+  const int nrows = nch * CH;
+  const int P = nrows >= 256 ? 1 : (nrows >= 128 ? 2 : (nrows >= 64 ? 4 : 8));
+  const float2* rp0 = rowpart + ((size_t)b * d.Hkv + g) * d.ns1 * d.R;
+  auto row_of = [&](int lr) { return lr < nrows ? row0 + (lr / CH) * cstep + (lr % CH) : d.R; };
+  float2 pre[2][8];
+  {
+    const int p = tid % P;
+    const float2* rp = rp0 + min(row_of(tid / P), d.R - 1);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) pre[h][j] = rp[(size_t)min(p + (8 * h + j) * P, d.ns1 - 1) * d.R];
+  }
 
   // The keys, the first two chunks and the keep byte of the thread's key are
-  // all in flight together; the keep bytes go last (their first use waits
-  // for them and, loads completing in order, for everything before them).
+  // in flight while the row statistics are merged.
   Ring ring;
-  ring.init(q, rowstat, b, g, d, w, lane, row0, cstep);
+  ring.init(q, b, g, d, w, lane, row0, cstep);
   Tile tile;
   tile.init(lane);
   tile.load_keys(k + (((size_t)b * d.S + min(key0, d.V_full - 1)) * d.Hkv + g) * Tile::RB,
                  (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.V_full - key0)), lane);
-  ring.issue(lds, w, lane);
-  if (nch > 1) ring.issue(lds + Ring::BUFB, w, lane);
+  ring.issue(lds, w);
+  if (nch > 1) ring.issue(lds + Ring::CB, w);
   asm volatile("" ::: "memory");  // keep the copies ahead of the keep-byte load
   const int tkey = vt * KT + tid;
-  const bool tkept = tkey < d.V_full && (keep_row == nullptr || keep_row[min(tkey, d.V_full - 1)]);
-  // the flag words of block_any sit past the chunk buffers, which are being filled
-  if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds + Ring::BYTES))) {
-    // no kept key in the tile: its column mass is 0 (the copies into LDS
-    // land before the workgroup ends)
+  const uint8_t tkb = keep_row ? keep_row[min(tkey, d.V_full - 1)] : 1;
+
+  // fold splits s0 + j*P (j < 8; those past ns1 ignored) into a running (max, sum)
+  auto fold8 = [&](float2 (&u)[8], int s0, float& m, float& z) {
+    float mg = m;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      if (s0 + j * P >= d.ns1) u[j] = make_float2(-INFINITY, 0.f);
+      mg = fmaxf(mg, u[j].x);
+    }
+    if (mg != -INFINITY) {
+      // exp2(-inf - mg) = 0 for splits without a visible key (their sum is 0)
+      z = m == -INFINITY ? 0.f : z * exp2f(m - mg);
+#pragma unroll
+      for (int j = 0; j < 8; ++j) z += u[j].y * exp2f(u[j].x - mg);
+      m = mg;
+    }
+  };
+  for (int base = 0; base < nrows * P; base += 256) {
+    const int idx = base + tid, lr = idx / P, p = idx - lr * P;
+    const int r = row_of(lr);
+    float m = -INFINITY, z = 0.f;
+    int s0 = p;
+    if (base == 0) {
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        fold8(pre[h], s0, m, z);
+        s0 += 8 * P;
+      }
+    }
+    if (r < d.R) {
+      const float2* rp = rp0 + r;
+      for (; s0 < d.ns1; s0 += 8 * P) {
+        float2 u[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) u[j] = rp[(size_t)min(s0 + j * P, d.ns1 - 1) * d.R];
+        fold8(u, s0, m, z);
+      }
+    }
+    for (int off = 1; off < P; off <<= 1) {
+      const float mo = __shfl_xor(m, off), zo = __shfl_xor(z, off);
+      const float mn = fmaxf(m, mo);
+      z = (m == -INFINITY ? 0.f : z * exp2f(m - mn)) + (mo == -INFINITY ? 0.f : zo * exp2f(mo - mn));
+      m = mn;
+    }
+    // rows past R: exp2(-inf) = 0 and a zero weight
+    if (p == 0 && lr < nrows) table[lr] = r < d.R ? make_float2(-m, 1.0f / z) : make_float2(-INFINITY, 0.f);
+  }
+
+  const bool tkept = tkey < d.V_full && tkb != 0;
+  if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds + FLG))) {
+    // no kept key in the tile: nothing to add (the copies into LDS land
+    // before the workgroup ends)
     wait_vmcnt<0>();
-    if (tkey < d.V_full) out[tkey] = 0.f;
     return;
   }
   const float c = d.scale_log2;
   const int cpw = __builtin_amdgcn_readfirstlane(Ring::copies(w));  // wave-uniform: scalar branches
 
   // four partial sums per key column (accumulator rows r with r % 4 = j)
-  float acc[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+  float cm[2][4] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
 
   // Chunk i sits in buffer i % 3. Step i waits for its copies (those of chunk
   // i+1 may stay in flight; loads complete in order), and its barrier also
   // marks the end of every read of chunk i-1, whose buffer then takes chunk i+2.
   auto body = [&](auto bufc, int i) {
     constexpr int BUF = decltype(bufc)::value;
-    const uint8_t* buf = lds + BUF * Ring::BUFB;
+    const uint8_t* buf = lds + BUF * Ring::CB;
     wait_vmcnt_upto(i + 1 < nch ? cpw : 0);
     lds_barrier();
-    if (i + 2 < nch) ring.issue(lds + ((BUF + 2) % Ring::NBUF) * Ring::BUFB, w, lane);
+    if (i + 2 < nch) ring.issue(lds + ((BUF + 2) % Ring::NBUF) * Ring::CB, w);
     f32x16 s[2];
     tile.logits(buf, lane, s);
     // (-max, 1/sum) of the lane's accumulator rows 8*j + 4*hl + 0..3
     f32x4 st[8];
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const f32x4* sp = reinterpret_cast<const f32x4*>(buf + Ring::CB + (8 * j + 4 * hl) * 8);
+      const f32x4* sp = reinterpret_cast<const f32x4*>(table + i * CH + 8 * j + 4 * hl);
       st[2 * j] = sp[0];
       st[2 * j + 1] = sp[1];
-    }
-    const int valid = d.R - (row0 + i * cstep);  // rows of this chunk below R
-    if (valid < CH) {
-      // rows past R: exp2(-inf) = 0 and a zero weight
-#pragma unroll
-      for (int r = 0; r < 16; ++r)
-        if (acc_row(r, hl) >= valid) {
-          if (r & 1) { st[r >> 1].z = -INFINITY; st[r >> 1].w = 0.f; }
-          else { st[r >> 1].x = -INFINITY; st[r >> 1].y = 0.f; }
-        }
     }
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
@@ -954,7 +959,7 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
       for (int r = 0; r < 16; ++r) {
         const float ms = (r & 1) ? st[r >> 1].z : st[r >> 1].x;
         const float iz = (r & 1) ? st[r >> 1].w : st[r >> 1].y;
-        acc[nb][r & 3] = fmaf(__builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms)), iz, acc[nb][r & 3]);
+        cm[nb][r & 3] = fmaf(__builtin_amdgcn_exp2f(fmaf(s[nb][r], c, ms)), iz, cm[nb][r & 3]);
       }
   };
   for (int i = 0; i < nch; i += 3) {
@@ -966,42 +971,16 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   // lane L ends with key key0 + L
   float tot[2];
 #pragma unroll
-  for (int nb = 0; nb < 2; ++nb) tot[nb] = (acc[nb][0] + acc[nb][1]) + (acc[nb][2] + acc[nb][3]);
+  for (int nb = 0; nb < 2; ++nb) tot[nb] = (cm[nb][0] + cm[nb][1]) + (cm[nb][2] + cm[nb][3]);
   const float give = hl ? tot[0] : tot[1];
   const float got = __shfl_xor(give, 32);
   const float colmass = (hl ? tot[1] : tot[0]) + got;
   const int key = key0 + lane;
-  if (key < d.V_full) {
-    // dropped keys were summed over too; their column is forced to 0
-    const bool kept = keep_row == nullptr || keep_row[key];
-    out[key] = kept ? colmass : 0.f;
-  }
+  // dropped keys were summed over too; their column stays 0
+  if (key < d.V_full && (keep_row == nullptr || keep_row[key]))
+    __hip_atomic_fetch_add(acc + (size_t)b * d.V_full + key, (unsigned long long)__float2ll_rn(colmass * d.fx),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-
-// ---------------------------------------------------------------- column sum
-// scores[b][j] = (sum over KV groups g and row splits of colpart[b][g][split][j],
-// in that order) / (Hq*T) for kept visual tokens, -inf for dropped ones.
-
-__global__ void __launch_bounds__(256)
-score_colsum_kernel(int S, int V_full, int nparts, float count, const float* __restrict__ colpart,
-                    const uint8_t* __restrict__ token_keep, float* __restrict__ scores) {
-  const int b = blockIdx.y, j = blockIdx.x * 256 + threadIdx.x;
-  if (j >= V_full) return;
-  const float* cp = colpart + (size_t)b * nparts * V_full + j;
-  float v[8];
-  float sum = 0.f;
-  int p = 0;
-  for (; p + 8 <= nparts; p += 8) {
-#pragma unroll
-    for (int u = 0; u < 8; ++u) v[u] = cp[(size_t)(p + u) * V_full];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) sum += v[u];
-  }
-  for (; p < nparts; ++p) sum += cp[(size_t)p * V_full];
-  const bool kept = token_keep == nullptr || token_keep[(size_t)b * S + j];
-  scores[(size_t)b * V_full + j] = kept ? sum / count : -INFINITY;
-}
-
 
 // ---------------------------------------------------------------- top-k + compaction
 
@@ -1083,13 +1062,14 @@ __device__ __forceinline__ int block_scan_excl(int v, int* wsum, int* total) {
 }
 
 // One workgroup per sample: the compacted offset from every earlier sample's
-// kept-visual count, order keys of the scores, radix select of the k_b-th
-// largest key (12-bit digits below the common prefix of the kept keys), then
-// the stable compaction.
+// kept-visual count, the scores (fixed-point column sums times inv: the mean
+// over the Hq*T text rows; -inf for dropped tokens), their order keys, radix
+// select of the k_b-th largest key (12-bit digits below the common prefix of
+// the kept keys), then the stable compaction.
 __global__ void __launch_bounds__(kTopkThreads)
 topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restrict__ token_keep,
-                    const float* __restrict__ scores, int32_t* __restrict__ kept_index,
-                    int32_t* __restrict__ cu_seqlens) {
+                    const unsigned long long* __restrict__ acc, double inv, float* __restrict__ scores,
+                    int32_t* __restrict__ kept_index, int32_t* __restrict__ cu_seqlens) {
   __shared__ uint32_t keys[LITEVLM_MAX_VISUAL];
   __shared__ int hist[kBins];
   __shared__ int vcnt[LITEVLM_MAX_BATCH];
@@ -1111,28 +1091,35 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   // are >= 0x80000000 since scores are >= 0); loads are unconditional from
   // clamped addresses so that a thread's rounds are all in flight at once.
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * S : nullptr;
-  const float* sc = scores + (size_t)b * V_full;
+  const unsigned long long* ac = acc + (size_t)b * V_full;
+  float* sc = scores + (size_t)b * V_full;
+  auto score_of = [&](unsigned long long v, bool kept) { return kept ? (float)((double)v * inv) : -INFINITY; };
   uint32_t kmin = 0xFFFFFFFFu, kmax = 0u;
   const bool vec = V_full >= 4 && (V_full & 3) == 0 && (reinterpret_cast<uintptr_t>(sc) & 15) == 0 &&
+                   (reinterpret_cast<uintptr_t>(ac) & 15) == 0 &&
                    (keep_row == nullptr || (reinterpret_cast<uintptr_t>(keep_row) & 3) == 0);
   if (vec) {
+    typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
     constexpr int R4 = LITEVLM_MAX_VISUAL / (4 * kTopkThreads);
-    float4 s4[R4];
+    u64x2 a4[R4][2];
     uint32_t f4[R4];
 #pragma unroll
     for (int i = 0; i < R4; ++i) {
       const int j4 = min(4 * (tid + i * kTopkThreads), V_full - 4);
-      s4[i] = *reinterpret_cast<const float4*>(sc + j4);
+      a4[i][0] = *reinterpret_cast<const u64x2*>(ac + j4);
+      a4[i][1] = *reinterpret_cast<const u64x2*>(ac + j4 + 2);
       f4[i] = keep_row ? *reinterpret_cast<const uint32_t*>(keep_row + j4) : 0x01010101u;
     }
 #pragma unroll
     for (int i = 0; i < R4; ++i) {
       const int j4 = 4 * (tid + i * kTopkThreads);
       if (j4 < V_full) {
-        const float sv[4] = {s4[i].x, s4[i].y, s4[i].z, s4[i].w};
+        const unsigned long long av[4] = {a4[i][0].x, a4[i][0].y, a4[i][1].x, a4[i][1].y};
+        float sv[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const bool kept = ((f4[i] >> (8 * u)) & 0xFFu) != 0u;
+          sv[u] = score_of(av[u], kept);
           const uint32_t key = kept ? order_key(sv[u]) : 0u;
           if (kept) {
             kmin = min(kmin, key);
@@ -1140,12 +1127,15 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
           }
           keys[j4 + u] = key;
         }
+        *reinterpret_cast<float4*>(sc + j4) = make_float4(sv[0], sv[1], sv[2], sv[3]);
       }
     }
   } else {
     for (int j = tid; j < V_full; j += kTopkThreads) {
       const bool kept = keep_row == nullptr || keep_row[j];
-      const uint32_t key = kept ? order_key(sc[j]) : 0u;
+      const float sv = score_of(ac[j], kept);
+      sc[j] = sv;
+      const uint32_t key = kept ? order_key(sv) : 0u;
       if (kept) {
         kmin = min(kmin, key);
         kmax = max(kmax, key);
@@ -1359,8 +1349,9 @@ static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
   // (sample, KV group, row block) are split until the grid has ~256
   // workgroups, at most kMaxSplitTiles tiles to one split. Sweep 2: row chunks
   // are split over workgroups while the grid fits one pass of the chip at
-  // three 4-wave workgroups per CU, at most 4 ways since every split
-  // multiplies the column partials the column sum reads.
+  // three 4-wave workgroups per CU, at most 4 ways (every split merges its
+  // rows' statistics again and adds its own column partials), and at least
+  // as many ways as keep a workgroup within kMaxChunksPerSplit chunks.
   ScoreSplit p;
   const int T = S - V_full;
   const int R = (Hq / Hkv) * T;
@@ -1372,7 +1363,8 @@ static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
   p.n_vt = (V_full + KT - 1) / KT;
   p.nchunks = (R + CH - 1) / CH;
   const long long c2 = (long long)p.n_vt * Hkv * B;
-  p.rs2 = c2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4), std::max<long long>(1, 768 / c2));
+  const int fit = c2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4), std::max<long long>(1, 768 / c2));
+  p.rs2 = std::max(fit, (p.nchunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit);
   return p;
 }
 
@@ -1381,9 +1373,8 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv)
   const size_t R = (size_t)(Hq / Hkv) * (S - V_full);
   ScoreWorkspace w;
   w.rowpart_off = 0;
-  w.rowstat_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1 * R);
-  w.colpart_off = align256(w.rowstat_off + sizeof(float2) * B * Hkv * R);
-  w.total = align256(w.colpart_off + sizeof(float) * B * Hkv * (size_t)sp.rs2 * V_full);
+  w.acc_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1 * R);
+  w.total = align256(w.acc_off + sizeof(unsigned long long) * B * (size_t)V_full);
   return w;
 }
 
@@ -1391,19 +1382,13 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv)
 static int sweep_grid(long long ncol, int nsplit) { return (int)(8 * ((ncol + 7) / 8) * nsplit); }
 
 template <int DT, int D>
-static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp,
-                          float2* rowpart, float2* rowstat, float* colpart, hipStream_t stream) {
+static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp, float2* rowpart,
+                          unsigned long long* acc, hipStream_t stream) {
   hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_rb, sp.ns1)),
-                     dim3(kSweepThreads), 0, stream, d, a.q, a.k, a.token_keep, rowpart);
-  const int rows_total = a.B * a.Hkv * d.R;
-  hipLaunchKernelGGL(sp.ns1 <= 4 * kMergeMax ? score_rowmerge_kernel<true> : score_rowmerge_kernel<false>,
-                     dim3((rows_total + 63) / 64), dim3(256), 0, stream, rows_total, d.R, sp.ns1, rowpart, rowstat);
-  if (sp.n_vt > 0) {
+                     dim3(kSweepThreads), 0, stream, d, a.q, a.k, a.token_keep, rowpart, acc);
+  if (sp.n_vt > 0)
     hipLaunchKernelGGL((score_colmass_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_vt, sp.rs2)),
-                       dim3(64 * kColWaves), 0, stream, d, a.q, a.k, a.token_keep, rowstat, colpart);
-    hipLaunchKernelGGL(score_colsum_kernel, dim3((a.V_full + 255) / 256, a.B), dim3(256), 0, stream, a.S,
-                       a.V_full, a.Hkv * sp.rs2, (float)a.Hq * (float)d.T, colpart, a.token_keep, a.scores);
-  }
+                       dim3(64 * kColWaves), 0, stream, d, a.q, a.k, a.token_keep, rowpart, acc);
 }
 
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
@@ -1411,8 +1396,7 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   const ScoreSplit sp = score_split(a.B, a.S, a.V_full, a.Hq, a.Hkv);
   char* ws = static_cast<char*>(a.workspace);
   float2* rowpart = reinterpret_cast<float2*>(ws + w.rowpart_off);
-  float2* rowstat = reinterpret_cast<float2*>(ws + w.rowstat_off);
-  float* colpart = reinterpret_cast<float*>(ws + w.colpart_off);
+  unsigned long long* acc = reinterpret_cast<unsigned long long*>(ws + w.acc_off);
   ScoreDims d;
   d.B = a.B;
   d.S = a.S;
@@ -1429,17 +1413,24 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.nchunks = sp.nchunks;
   d.rs2 = sp.rs2;
   d.scale_log2 = a.logit_scale_log2;
+  // A text row adds at most 1 to a column, so a column sum is at most Hq*T:
+  // with Hq*T <= 2^e, fx = 2^(62-e) keeps every sum below 2^62.
+  const double rows = (double)a.Hq * (double)d.T;
+  int e = 0;
+  while (std::ldexp(1.0, e) < rows) ++e;
+  d.fx = std::ldexp(1.0f, 62 - e);
+  const double inv = 1.0 / ((double)d.fx * rows);
 
-#define LITEVLM_SWEEPS(DT)                                                             \
-  (a.D == 128 ? launch_sweeps<DT, 128>(a, d, sp, rowpart, rowstat, colpart, stream) \
-              : launch_sweeps<DT, 64>(a, d, sp, rowpart, rowstat, colpart, stream))
+#define LITEVLM_SWEEPS(DT)                                           \
+  (a.D == 128 ? launch_sweeps<DT, 128>(a, d, sp, rowpart, acc, stream) \
+              : launch_sweeps<DT, 64>(a, d, sp, rowpart, acc, stream))
   if (a.dtype == LITEVLM_BF16) LITEVLM_SWEEPS(LITEVLM_BF16);
   else if (a.dtype == LITEVLM_FP8_E4M3) LITEVLM_SWEEPS(LITEVLM_FP8_E4M3);
   else LITEVLM_SWEEPS(LITEVLM_F32);
 #undef LITEVLM_SWEEPS
 
   hipLaunchKernelGGL(topk_compact_kernel, dim3(a.B), dim3(kTopkThreads), 0, stream, a.S, a.V_full,
-                     a.keep_ratio, a.token_keep, a.scores, a.kept_index, a.cu_seqlens);
+                     a.keep_ratio, a.token_keep, acc, inv, a.scores, a.kept_index, a.cu_seqlens);
   if (a.qc || a.kc || a.vc) {
     const int esz = a.dtype == LITEVLM_F32 ? 4 : (a.dtype == LITEVLM_BF16 ? 2 : 1);
     const int qvec = a.Hq * a.D * esz / 16, kvvec = a.Hkv * a.D * esz / 16;
