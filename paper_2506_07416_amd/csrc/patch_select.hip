@@ -11,22 +11,25 @@ patch_select_kernel(int N, int S, ViewOffsets vo, const float* __restrict__ logi
                     const float* __restrict__ lexical, float w, float tau,
                     uint8_t* __restrict__ view_keep, uint8_t* __restrict__ token_keep,
                     int32_t* __restrict__ n_visual_kept) {
-  const int b = blockIdx.x;
+  const int b = blockIdx.x, tid = threadIdx.x;
   __shared__ uint8_t keep_s[LITEVLM_MAX_VIEWS];
   __shared__ float s_s[LITEVLM_MAX_VIEWS];
+  __shared__ int off_s[LITEVLM_MAX_VIEWS + 1];
+  // the view offsets go to LDS once, so that no loop below waits on a
+  // dependent load of them
+  if (tid <= N) off_s[tid] = vo.off[tid];
   // One thread per view, written as the definition reads: no FMA
   // contraction and IEEE division, so the decision matches an fp32 evaluation.
-  if (threadIdx.x < N) {
-    const int v = threadIdx.x;
-    const float x = logit[b * N + v];
+  if (tid < N) {
+    const float x = logit[b * N + tid];
     const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-x)));
-    const float lex = lexical ? lexical[b * N + v] : 0.0f;
+    const float lex = lexical ? lexical[b * N + tid] : 0.0f;
     const float s = __fadd_rn(__fmul_rn(w, lex), __fmul_rn(__fsub_rn(1.0f, w), sig));
-    s_s[v] = s;
-    keep_s[v] = (uint8_t)(s > tau);
+    s_s[tid] = s;
+    keep_s[tid] = (uint8_t)(s > tau);
   }
   __syncthreads();
-  if (threadIdx.x == 0) {
+  if (tid == 0) {
     // if no view passes, keep the best one (lowest index among equal scores)
     int any = 0, best_v = 0;
     for (int v = 0; v < N; ++v) {
@@ -36,21 +39,43 @@ patch_select_kernel(int N, int S, ViewOffsets vo, const float* __restrict__ logi
     if (!any) keep_s[best_v] = 1;
   }
   __syncthreads();
-  if (threadIdx.x < N) view_keep[b * N + threadIdx.x] = keep_s[threadIdx.x];
-  if (threadIdx.x == 0 && n_visual_kept) {
+  if (tid < N) view_keep[b * N + tid] = keep_s[tid];
+  if (tid == 0 && n_visual_kept) {
     int nvis = 0;
     for (int v = 0; v < N; ++v)
-      if (keep_s[v]) nvis += vo.off[v + 1] - vo.off[v];
+      if (keep_s[v]) nvis += off_s[v + 1] - off_s[v];
     n_visual_kept[b] = nvis;
   }
-  __syncthreads();
-  const int V_full = vo.off[N];
+  // token mask: visual token p takes its view's flag (views are contiguous
+  // and view-major), text tokens are 1; 16 bytes per thread and store
   uint8_t* row = token_keep + (size_t)b * S;
-  for (int v = 0; v < N; ++v) {
-    const uint8_t k = keep_s[v];
-    for (int p = vo.off[v] + threadIdx.x; p < vo.off[v + 1]; p += blockDim.x) row[p] = k;
+  const bool vec = (reinterpret_cast<uintptr_t>(row) & 15) == 0;
+  for (int p0 = 16 * tid; p0 < S; p0 += 16 * 256) {
+    // view of p0: the number of views ending at or before it (N independent
+    // LDS reads rather than a dependent walk); v == N for text tokens
+    int v = 0;
+    for (int u = 0; u < N; ++u) v += p0 >= off_s[u + 1] ? 1 : 0;
+    const int n = min(16, S - p0);
+    uint32_t wd[4];
+    if (p0 + n <= (v < N ? off_s[v + 1] : S)) {
+      // the whole chunk lies in one view (or in the text)
+      const uint32_t k = v < N ? keep_s[v] : 1u;
+      wd[0] = wd[1] = wd[2] = wd[3] = k * 0x01010101u;
+    } else {
+      wd[0] = wd[1] = wd[2] = wd[3] = 0u;
+      for (int j = 0; j < n; ++j) {
+        const int p = p0 + j;
+        while (v < N && p >= off_s[v + 1]) ++v;
+        const uint32_t k = v < N ? keep_s[v] : 1u;
+        wd[j >> 2] |= k << (8 * (j & 3));
+      }
+    }
+    if (vec && n == 16) {
+      *reinterpret_cast<uint4*>(row + p0) = make_uint4(wd[0], wd[1], wd[2], wd[3]);
+    } else {
+      for (int j = 0; j < n; ++j) row[p0 + j] = (uint8_t)(wd[j >> 2] >> (8 * (j & 3)));
+    }
   }
-  for (int p = V_full + threadIdx.x; p < S; p += blockDim.x) row[p] = 1;
 }
 
 hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const float* logit,
