@@ -7,6 +7,7 @@
  * Three calls, in pipeline order, all enqueued on one HIP stream:
  *   litevlm_patch_select      view selection and per-view patch masking
  *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
+ *                             (litevlm_token_score_topk_rows: the last n text rows only)
  *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
  *
  * Conventions shared by every call
@@ -157,6 +158,38 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
                                           double keep_ratio, float* scores, int32_t* kept_index,
                                           int32_t* cu_seqlens, void* qc, void* kc, void* vc,
                                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Bytes of device workspace litevlm_token_score_topk_rows needs for these
+ * sizes (0 when the sizes or query_rows are invalid). */
+size_t litevlm_token_score_topk_rows_workspace(int32_t B, int32_t S, int32_t V_full,
+                                               int32_t Hq, int32_t Hkv, int32_t D,
+                                               int32_t query_rows);
+
+/*
+ * litevlm_token_score_topk_rows - litevlm_token_score_topk with only the last
+ * query_rows text tokens as query rows.
+ *
+ * Paper: Related Work, Visual Token Compression (FastV prunes visual tokens by
+ * the attention that the last token pays them, inside the LLM after an early
+ * layer); the scoring of litevlm_token_score_topk is otherwise unchanged.
+ *
+ *   score_b(j) = 1/(Hq*n) * sum_h sum_{t = T-n}^{T-1} softmax(...)[j], n = query_rows,
+ * with the rows, masks, k_b rule, top-k order and compaction exactly as in
+ * litevlm_token_score_topk (the compacted sequence still keeps every text
+ * token). query_rows = 1 is the last-token readout; query_rows = T is
+ * litevlm_token_score_topk. query_rows outside 1..T gives LITEVLM_ERR_BAD_VALUE.
+ * The workspace comes from litevlm_token_score_topk_rows_workspace(); every
+ * other argument, its layout, ownership and errors are those of
+ * litevlm_token_score_topk.
+ */
+litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                               int32_t Hq, int32_t Hkv, int32_t D, int32_t query_rows,
+                                               const void* q, const void* k, const void* v,
+                                               float softmax_scale, float q_scale, float k_scale,
+                                               float v_scale, const uint8_t* token_keep,
+                                               double keep_ratio, float* scores, int32_t* kept_index,
+                                               int32_t* cu_seqlens, void* qc, void* kc, void* vc,
+                                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
  * litevlm_prefill_attn - causal GQA prefill attention over packed sequences.

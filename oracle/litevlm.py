@@ -108,7 +108,7 @@ def patch_selected_positions(token_keep_b: np.ndarray, V_full: int) -> np.ndarra
 # --------------------------------------------------------------------------- token scoring
 
 def token_scores(q: np.ndarray, k: np.ndarray, token_keep: np.ndarray, V_full: int,
-                 Hq: int, Hkv: int, scale: float) -> np.ndarray:
+                 Hq: int, Hkv: int, scale: float, query_rows: Optional[int] = None) -> np.ndarray:
     """Visual-token importance (Design section, Token Selection Module
     paragraph: a standalone copy of the first decoder layer scores visual
     tokens in the manner of FastV, i.e. from self-attention, Related Work,
@@ -122,10 +122,18 @@ def token_scores(q: np.ndarray, k: np.ndarray, token_keep: np.ndarray, V_full: i
     included; no renormalisation over visual keys). The score of visual token j
     is the sum of those rows' entries at j over all (h, t), divided by Hq*T.
     Tokens of dropped views score -inf. q, k: float64 [B, S, H, D].
+
+    query_rows = n keeps only the last n text tokens as query rows (divided by
+    Hq*n instead): n = 1 is the FastV-style readout from the last token
+    (Related Work, Visual Token Compression: FastV prunes by the attention the
+    last token pays); n = T (the default) is the reading above.
     Returns float64 [B, V_full].
     """
     B, S = token_keep.shape
     T = S - V_full
+    n = T if query_rows is None else int(query_rows)
+    if not 1 <= n <= T:
+        raise ValueError("query_rows must lie in 1..T")
     G = Hq // Hkv
     out = np.full((B, V_full), -np.inf)
     for b in range(B):
@@ -133,11 +141,12 @@ def token_scores(q: np.ndarray, k: np.ndarray, token_keep: np.ndarray, V_full: i
         V_b = idx.shape[0] - T
         S_b = idx.shape[0]
         acc = np.zeros(V_b)
-        p = V_b + np.arange(T)                       # text row positions in the selected sequence
+        tq = np.arange(T - n, T)                     # the query text tokens
+        p = V_b + tq                                 # their positions in the selected sequence
         blocked = np.arange(S_b)[None, :] > p[:, None]
         for h in range(Hq):
             g = h // G
-            qt = q[b, V_full + np.arange(T), h, :]   # [T, D] text query rows
+            qt = q[b, V_full + tq, h, :]             # [n, D] text query rows
             kp = k[b, idx, g, :]                     # [S_b, D] keys of the selected sequence
             logits = (qt @ kp.T) * scale
             logits[blocked] = -np.inf
@@ -145,7 +154,7 @@ def token_scores(q: np.ndarray, k: np.ndarray, token_keep: np.ndarray, V_full: i
             e = np.exp(logits)
             prob = e / e.sum(axis=1, keepdims=True)
             acc += prob[:, :V_b].sum(axis=0)
-        out[b, idx[:V_b]] = acc / (Hq * T)
+        out[b, idx[:V_b]] = acc / (Hq * n)
     return out
 
 
@@ -240,16 +249,17 @@ def prefill_attention(qc: np.ndarray, kc: np.ndarray, vc: np.ndarray, cu_seqlens
 # --------------------------------------------------------------------------- whole path
 
 def run_path(case, keep_ratio: Optional[float] = None, attention: bool = True,
-             attention_rows: Optional[Sequence[int]] = None) -> dict:
+             attention_rows: Optional[Sequence[int]] = None, query_rows: Optional[int] = None) -> dict:
     """All steps in order on a synthetic case: patch select, patch-selected
-    scoring, k rule, top-k, compaction, gather, prefill attention."""
+    scoring (over the last query_rows text tokens; all of them by default),
+    k rule, top-k, compaction, gather, prefill attention."""
     r = case.keep_ratio if keep_ratio is None else keep_ratio
     q, k, v = decode_inputs(case)
     scale = 1.0 / math.sqrt(case.D)
     view_keep = patch_select(case.view_logit, case.view_lexical, case.w_lexical, case.threshold)
     tk = token_keep_from_views(view_keep, case.view_offsets, case.S)
     V_b = tk[:, :case.V_full].sum(axis=1).astype(np.int64)
-    scores = token_scores(q, k, tk, case.V_full, case.Hq, case.Hkv, scale)
+    scores = token_scores(q, k, tk, case.V_full, case.Hq, case.Hkv, scale, query_rows=query_rows)
     k_b = np.array([keep_count(r, int(n)) for n in V_b], np.int64)
     selected = [select_topk(scores[b], tk[b], case.V_full, int(k_b[b])) for b in range(case.B)]
     kept_index, cu = compact(selected, case.V_full, case.S)

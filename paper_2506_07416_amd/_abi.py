@@ -26,6 +26,10 @@ SIGNATURES = {
     "litevlm_token_score_topk": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp,
                                         _f32, _f32, _f32, _f32, _vp, _f64, _vp, _vp, _vp, _vp, _vp,
                                         _vp, _vp, _sz, _vp]),
+    "litevlm_token_score_topk_rows_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32, _i32]),
+    "litevlm_token_score_topk_rows": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
+                                             _vp, _f32, _f32, _f32, _f32, _vp, _f64, _vp, _vp, _vp,
+                                             _vp, _vp, _vp, _vp, _sz, _vp]),
     "litevlm_prefill_attn": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32,
                                     _f32, _f32, _f32, _f32, _i32, _vp, _vp]),
 }

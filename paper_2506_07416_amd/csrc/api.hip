@@ -73,25 +73,32 @@ litevlm_status_t litevlm_patch_select(int32_t B, int32_t N, int32_t S,
                                         static_cast<hipStream_t>(stream)));
 }
 
-size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full, int32_t Hq,
-                                          int32_t Hkv, int32_t D) {
+size_t litevlm_token_score_topk_rows_workspace(int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                               int32_t Hkv, int32_t D, int32_t query_rows) {
   if (check_score_shape(B, S, V_full, Hq, Hkv, D) != LITEVLM_OK) return 0;
-  return score_workspace_layout(B, S, V_full, Hq, Hkv).total;
+  if (query_rows < 1 || query_rows > S - V_full) return 0;
+  return score_workspace_layout(B, S, V_full, Hq, Hkv, query_rows).total;
 }
 
-litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
-                                          int32_t Hq, int32_t Hkv, int32_t D, const void* q,
-                                          const void* k, const void* v, float softmax_scale,
-                                          float q_scale, float k_scale, float v_scale,
-                                          const uint8_t* token_keep, double keep_ratio,
-                                          float* scores, int32_t* kept_index, int32_t* cu_seqlens,
-                                          void* qc, void* kc, void* vc, void* workspace,
-                                          size_t workspace_bytes, void* stream) {
+size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                          int32_t Hkv, int32_t D) {
+  return litevlm_token_score_topk_rows_workspace(B, S, V_full, Hq, Hkv, D, S - V_full);
+}
+
+litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                               int32_t Hq, int32_t Hkv, int32_t D, int32_t query_rows,
+                                               const void* q, const void* k, const void* v,
+                                               float softmax_scale, float q_scale, float k_scale,
+                                               float v_scale, const uint8_t* token_keep, double keep_ratio,
+                                               float* scores, int32_t* kept_index, int32_t* cu_seqlens,
+                                               void* qc, void* kc, void* vc, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
   if (!q || !k || !scores || !kept_index || !cu_seqlens) return LITEVLM_ERR_NULL_POINTER;
   if (vc && !v) return LITEVLM_ERR_NULL_POINTER;
   if (!valid_dtype(dtype)) return LITEVLM_ERR_UNSUPPORTED;
   const litevlm_status_t sh = check_score_shape(B, S, V_full, Hq, Hkv, D);
   if (sh != LITEVLM_OK) return sh;
+  if (query_rows < 1 || query_rows > S - V_full) return LITEVLM_ERR_BAD_VALUE;
   if (!finite_pos(softmax_scale) || !finite_pos(q_scale) || !finite_pos(k_scale) ||
       !finite_pos(v_scale))
     return LITEVLM_ERR_BAD_VALUE;
@@ -103,7 +110,7 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
     if (p && !aligned(p, 16)) return LITEVLM_ERR_MISALIGNED;
   if (!aligned(scores, 4) || !aligned(kept_index, 4) || !aligned(cu_seqlens, 4))
     return LITEVLM_ERR_MISALIGNED;
-  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv).total;
+  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv, query_rows).total;
   if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
 
   ScoreArgs a;
@@ -114,6 +121,7 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.D = D;
+  a.query_rows = query_rows;
   a.q = q;
   a.k = k;
   a.v = v;
@@ -128,6 +136,21 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
   a.vc = vc;
   a.workspace = workspace;
   return hip_status(launch_token_score_topk(a, static_cast<hipStream_t>(stream)));
+}
+
+litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                          int32_t Hq, int32_t Hkv, int32_t D, const void* q,
+                                          const void* k, const void* v, float softmax_scale,
+                                          float q_scale, float k_scale, float v_scale,
+                                          const uint8_t* token_keep, double keep_ratio,
+                                          float* scores, int32_t* kept_index, int32_t* cu_seqlens,
+                                          void* qc, void* kc, void* vc, void* workspace,
+                                          size_t workspace_bytes, void* stream) {
+  // every text token is a query row (S > V_full is checked by the callee)
+  return litevlm_token_score_topk_rows(dtype, B, S, V_full, Hq, Hkv, D, S > V_full ? S - V_full : 1, q, k, v,
+                                       softmax_scale, q_scale, k_scale, v_scale, token_keep, keep_ratio,
+                                       scores, kept_index, cu_seqlens, qc, kc, vc, workspace, workspace_bytes,
+                                       stream);
 }
 
 litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32_t B, int32_t Hq,

@@ -21,15 +21,16 @@ hipError_t launch_patch_select(int B, int N, int S, const ViewOffsets& vo, const
 // Workspace of the scoring step, carved from one caller buffer:
 //   rowpart  float2 [B][Hkv][ns1][R]  per-key-split (max, sum) of each text row
 //   acc      u64    [B][V_full]       fixed-point column sums of sweep 2
-// with R = (Hq/Hkv)*T rows per KV group; ns1 (key splits of sweep 1) is a
-// function of the shape.
+// with R = (Hq/Hkv)*n_query rows per KV group (the last n_query text tokens
+// are the query rows); ns1 (key splits of sweep 1) is a function of the shape.
 struct ScoreWorkspace {
   size_t rowpart_off, acc_off, total;
 };
-ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv);
+ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv, int n_query);
 
 struct ScoreArgs {
   int dtype, B, S, V_full, Hq, Hkv, D;
+  int query_rows;  // the last query_rows text tokens are the query rows (1..T)
   const void* q;
   const void* k;
   const void* v;

@@ -51,6 +51,7 @@ struct ScoreSplit {
 
 struct ScoreDims {
   int B, S, V_full, T, Hq, Hkv, G, R;
+  int tq0;  // the query rows are text tokens tq0 .. tq0 + T - 1 (the last T of them)
   int n_rb, n_kt, ns1, n_vt, nchunks, rs2;
   float scale_log2;
   float fx;  // fixed-point scale of the column sums (a power of two)
@@ -444,7 +445,8 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
   const uint8_t* q = static_cast<const uint8_t*>(qv);
   const uint8_t* k = static_cast<const uint8_t*>(kv);
-  const QRows qr{q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * Tile::RB, d.G, d.Hq, Tile::RB, d.R};
+  const QRows qr{q + (((size_t)b * d.S + d.V_full + d.tq0) * d.Hq + (size_t)g * d.G) * Tile::RB, d.G, d.Hq,
+                 Tile::RB, d.R};
   const int row0 = rb * RBLK + 32 * w;
   const int row = row0 + lq;
   const bool wave_active = row0 < d.R;
@@ -497,7 +499,7 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   tile_flags(mw, keepl, kf, tile0, ntl, d.V_full, d.S, w, lane, live, plain);
 
   // token of the lane's row for the causal text mask (-1: a row past R sees no text)
-  const int t_row = row < d.R ? row / d.G : -1;
+  const int t_row = row < d.R ? d.tq0 + row / d.G : -1;
   const float c = d.scale_log2;
   float m_run = -INFINITY, z_run = 0.f;
 
@@ -742,7 +744,7 @@ struct QRing {
 
   __device__ __forceinline__ void init(const uint8_t* q, int b, int g, const ScoreDims& d, int w, int lane,
                                        int row0, int cstep) {
-    qbase = q + (((size_t)b * d.S + d.V_full) * d.Hq + (size_t)g * d.G) * RB;
+    qbase = q + (((size_t)b * d.S + d.V_full + d.tq0) * d.Hq + (size_t)g * d.G) * RB;
     G = d.G;
     Hq = d.Hq;
     T = d.T;
@@ -1344,7 +1346,7 @@ gather_rows_kernel(int B, int S, const int32_t* __restrict__ kept_index,
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
+static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv, int n_query) {
   // Sweep 1: one 16-wave workgroup per CU (256 CUs); the key tiles of each
   // (sample, KV group, row block) are split until the grid has ~256
   // workgroups, at most kMaxSplitTiles tiles to one split. Sweep 2: row chunks
@@ -1353,8 +1355,7 @@ static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
   // rows' statistics again and adds its own column partials), and at least
   // as many ways as keep a workgroup within kMaxChunksPerSplit chunks.
   ScoreSplit p;
-  const int T = S - V_full;
-  const int R = (Hq / Hkv) * T;
+  const int R = (Hq / Hkv) * n_query;
   p.n_rb = (R + RBLK - 1) / RBLK;
   p.n_kt = (S + KB - 1) / KB;
   const long long cols = std::max<long long>(1, (long long)B * Hkv * p.n_rb);
@@ -1368,9 +1369,9 @@ static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv) {
   return p;
 }
 
-ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv) {
-  const ScoreSplit sp = score_split(B, S, V_full, Hq, Hkv);
-  const size_t R = (size_t)(Hq / Hkv) * (S - V_full);
+ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv, int n_query) {
+  const ScoreSplit sp = score_split(B, S, V_full, Hq, Hkv, n_query);
+  const size_t R = (size_t)(Hq / Hkv) * n_query;
   ScoreWorkspace w;
   w.rowpart_off = 0;
   w.acc_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1 * R);
@@ -1392,8 +1393,8 @@ static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSpl
 }
 
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
-  const ScoreWorkspace w = score_workspace_layout(a.B, a.S, a.V_full, a.Hq, a.Hkv);
-  const ScoreSplit sp = score_split(a.B, a.S, a.V_full, a.Hq, a.Hkv);
+  const ScoreWorkspace w = score_workspace_layout(a.B, a.S, a.V_full, a.Hq, a.Hkv, a.query_rows);
+  const ScoreSplit sp = score_split(a.B, a.S, a.V_full, a.Hq, a.Hkv, a.query_rows);
   char* ws = static_cast<char*>(a.workspace);
   float2* rowpart = reinterpret_cast<float2*>(ws + w.rowpart_off);
   unsigned long long* acc = reinterpret_cast<unsigned long long*>(ws + w.acc_off);
@@ -1401,7 +1402,8 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.B = a.B;
   d.S = a.S;
   d.V_full = a.V_full;
-  d.T = a.S - a.V_full;
+  d.T = a.query_rows;
+  d.tq0 = a.S - a.V_full - a.query_rows;
   d.Hq = a.Hq;
   d.Hkv = a.Hkv;
   d.G = a.Hq / a.Hkv;

@@ -86,10 +86,16 @@ def st(dtype=_abi.BF16, B=1, S=100, V=80, Hq=8, Hkv=2, D=128, q=A, k=A, v=A, sm=
 def test_workspace_size():
     lib = lv.load()
     n = lib.litevlm_token_score_topk_workspace(1, 6272, 6144, 32, 8, 128)
-    # per-key-split row stats (at least one split) + merged row stats + per-group column mass
+    # per-key-split row stats (at least one split) + fixed-point column sums
     R = 4 * 128
-    assert n >= 8 * 8 * 1 * R + 8 * 8 * R + 4 * 8 * 6144
+    assert n >= 8 * 8 * 1 * R + 8 * 6144
     assert n % 256 == 0
+    # the rows variant with every text row needs exactly as much; fewer rows, less
+    assert lib.litevlm_token_score_topk_rows_workspace(1, 6272, 6144, 32, 8, 128, 128) == n
+    n1 = lib.litevlm_token_score_topk_rows_workspace(1, 6272, 6144, 32, 8, 128, 1)
+    assert 8 * 6144 <= n1 < n
+    assert lib.litevlm_token_score_topk_rows_workspace(1, 6272, 6144, 32, 8, 128, 0) == 0
+    assert lib.litevlm_token_score_topk_rows_workspace(1, 6272, 6144, 32, 8, 128, 129) == 0
     assert lib.litevlm_token_score_topk_workspace(1, 10, 10, 8, 2, 128) == 0    # no text token
     assert lib.litevlm_token_score_topk_workspace(1, 100, 80, 8, 3, 128) == 0   # Hq % Hkv
 
@@ -119,6 +125,22 @@ def test_token_score_topk_validation():
     assert st(ki=A + 2) == _abi.ERR_MISALIGNED
     assert st(ws=None) == _abi.ERR_WORKSPACE
     assert st(wsb=16) == _abi.ERR_WORKSPACE
+
+
+def test_token_score_topk_rows_validation():
+    lib = lv.load()
+
+    def rows(n, S=100, V=80, wsb=None, q=A):
+        if wsb is None:
+            wsb = lib.litevlm_token_score_topk_rows_workspace(1, S, V, 8, 2, 128, max(1, min(n, S - V)))
+        return lib.litevlm_token_score_topk_rows(_abi.BF16, 1, S, V, 8, 2, 128, n, q, A, A, 0.088, 1.0,
+                                                 1.0, 1.0, A, 0.5, A, A, A, A, A, A, A, wsb, None)
+    assert rows(0) == _abi.ERR_BAD_VALUE
+    assert rows(21) == _abi.ERR_BAD_VALUE                       # T = 20
+    assert rows(-3) == _abi.ERR_BAD_VALUE
+    assert rows(5, q=None) == _abi.ERR_NULL_POINTER
+    assert rows(5, S=80) == _abi.ERR_BAD_SHAPE                  # T = 0
+    assert rows(5, wsb=16) == _abi.ERR_WORKSPACE
 
 
 # ----------------------------------------------------------------------------- prefill_attn

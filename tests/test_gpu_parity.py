@@ -26,15 +26,17 @@ def attn_kind(dtype):
     return {"f32": "f32", "bf16": "bf16", "fp8": "fp8"}[dtype]
 
 
-def run_select(case, keep_ratio=None, gather=True):
-    """patch_select + token_score_topk on the GPU. Returns host copies."""
+def run_select(case, keep_ratio=None, gather=True, query_rows=None):
+    """patch_select + token_score_topk on the GPU (the rows variant when
+    query_rows is given). Returns host copies."""
     r = case.keep_ratio if keep_ratio is None else keep_ratio
     q, k, v = (to_device(x, case.dtype) for x in (case.q, case.k, case.v))
     logit = torch.from_numpy(case.view_logit).cuda()
     view_keep, token_keep, n_vis = lv.patch_select(logit, case.view_offsets, case.S,
                                                    case.w_lexical, case.threshold)
     out = lv.token_score_topk(q, k, v, token_keep, r, case.V_full, q_scale=case.q_scale,
-                              k_scale=case.k_scale, v_scale=case.v_scale, gather=gather)
+                              k_scale=case.k_scale, v_scale=case.v_scale, gather=gather,
+                              query_rows=query_rows)
     torch.cuda.synchronize()
     cu = out["cu_seqlens"].cpu().numpy()
     res = dict(view_keep=view_keep.cpu().numpy(), token_keep=token_keep.cpu().numpy(),
@@ -189,6 +191,44 @@ def test_select_chain_matches_oracle(name):
         ref_o = oracle.run_path(case)["o"]
         stats = check_attention(to_float64(o2), ref_o, attn_kind(case.dtype), name)
     log(f"  attention {stats}")
+
+
+# scoring from the last n text tokens only (n = 1: the last-token readout)
+ROWS_CASES = [
+    ("rows1-cfg2", dict(cfg=2), 1),
+    ("rows1-ragged-gqa", dict(cfg=4, Tv=100, T=37, keep_ratio=0.37), 1),
+    ("rows7-ragged-gqa", dict(cfg=4, run=1, Tv=96, T=37, keep_ratio=0.5), 7),
+    ("rows2-d64", dict(cfg=2, Tv=50, T=3, Hq=6, Hkv=3, D=64, keep_ratio=0.9), 2),
+    ("rows1-fp8", dict(cfg=5, Tv=128, T=32), 1),
+    ("rows1-f32", dict(cfg=1), 1),
+    ("rowsT-cfg2", dict(cfg=2, Tv=64, T=16), 16),
+]
+
+
+@pytest.mark.parametrize("name", [c[0] for c in ROWS_CASES])
+def test_select_query_rows_matches_oracle(name):
+    spec = {c[0]: c for c in ROWS_CASES}[name]
+    kw, n = dict(spec[1]), spec[2]
+    cfg = kw.pop("cfg")
+    case = synth.config_case(cfg, **kw)
+    log(f"select {name}: B={case.B} S={case.S} V={case.V_full} Hq={case.Hq} Hkv={case.Hkv} D={case.D} {case.dtype} r={case.keep_ratio} query rows {n}")
+    g = run_select(case, query_rows=n)
+    ref = oracle.run_path(case, attention=False, query_rows=n)
+    check_select(case, g, ref, name)
+    if n == case.S - case.V_full:
+        # every text row: the same call as litevlm_token_score_topk, bit for bit
+        g2 = run_select(case)
+        for key in ("scores", "kept_index", "cu"):
+            assert np.array_equal(g[key], g2[key]), key
+
+
+def test_cfg3_full_size_last_token():
+    # the last-token readout at the full 6x1024 + 128 shape
+    case = synth.config_case(3)
+    log("select cfg3 last token: S=6272 r=0.5")
+    g = run_select(case, keep_ratio=0.5, query_rows=1)
+    ref = oracle.run_path(case, keep_ratio=0.5, attention=False, query_rows=1)
+    check_select(case, g, ref, "cfg3-last-token")
 
 
 def test_chain_is_deterministic():

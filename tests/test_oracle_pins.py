@@ -33,11 +33,13 @@ def rand_qk(rng, B, S, Hq, Hkv, D, peaked=True):
     return q, k, v
 
 
-def sdpa_scores(q, k, token_keep, V_full, Hq, Hkv, scale):
+def sdpa_scores(q, k, token_keep, V_full, Hq, Hkv, scale, query_rows=None):
     """Importance scores read off torch's CPU float64 causal attention: with
-    identity value vectors, the output row of a query IS its probability row."""
+    identity value vectors, the output row of a query IS its probability row.
+    query_rows = n sums the rows of the last n text tokens only."""
     B, S = token_keep.shape
     T = S - V_full
+    n = T if query_rows is None else query_rows
     G = Hq // Hkv
     out = np.full((B, V_full), -np.inf)
     for b in range(B):
@@ -49,7 +51,7 @@ def sdpa_scores(q, k, token_keep, V_full, Hq, Hkv, scale):
         eye = torch.eye(S_b, dtype=torch.float64).expand(Hq, S_b, S_b)
         prob = torch.nn.functional.scaled_dot_product_attention(
             qq, kk, eye, is_causal=True, scale=scale)                        # [Hq, S_b, S_b]
-        mass = prob[:, V_b:, :V_b].sum(dim=(0, 1)).numpy() / (Hq * T)
+        mass = prob[:, V_b + T - n:, :V_b].sum(dim=(0, 1)).numpy() / (Hq * n)
         out[b, idx[:V_b]] = mass
     return out
 
@@ -277,6 +279,49 @@ def test_scores_hand_example():
     expect = [(p0[0] + p1[0]) / 2, (p0[1] + p1[1]) / 2]
     got = oracle.token_scores(q, k, np.ones((1, 4), np.uint8), 2, 1, 1, scale)
     assert np.allclose(got[0], expect, rtol=1e-14)
+
+
+@pytest.mark.parametrize("n", [1, 2, 5])
+def test_query_rows_scores_match_sdpa(n):
+    # FastV-style readout (the last n text tokens as the only query rows)
+    # against torch's float64 causal attention, with a dropped view
+    rng = np.random.default_rng(11 + n)
+    B, N, Tv, T, Hq, Hkv, D = 2, 3, 6, 5, 4, 2, 8
+    V_full, S = N * Tv, N * Tv + T
+    tk = np.ones((B, S), np.uint8)
+    tk[1, Tv:2 * Tv] = 0
+    q, k, _ = rand_qk(rng, B, S, Hq, Hkv, D)
+    scale = 1 / math.sqrt(D)
+    got = oracle.token_scores(q, k, tk, V_full, Hq, Hkv, scale, query_rows=n)
+    ref = sdpa_scores(q, k, tk, V_full, Hq, Hkv, scale, query_rows=n)
+    assert np.array_equal(np.isneginf(got), np.isneginf(ref))
+    fin = np.isfinite(ref)
+    assert np.allclose(got[fin], ref[fin], rtol=1e-12, atol=0)
+    if n == T:
+        assert np.array_equal(got, oracle.token_scores(q, k, tk, V_full, Hq, Hkv, scale))
+
+
+def test_query_rows_last_token_closed_form():
+    # Q = 0: the last token's row is uniform over its V_b + T visible keys, so
+    # every kept visual token scores 1/(V_b + T), and the all-tie selection is
+    # the lowest positions
+    B, N, Tv, T, Hq, Hkv, D = 1, 4, 8, 6, 4, 2, 8
+    V_full, S = N * Tv, N * Tv + T
+    tk = np.ones((B, S), np.uint8)
+    tk[0, 2 * Tv:3 * Tv] = 0
+    V_b = V_full - Tv
+    q = np.zeros((B, S, Hq, D))
+    k = np.random.default_rng(3).standard_normal((B, S, Hkv, D))
+    sc = oracle.token_scores(q, k, tk, V_full, Hq, Hkv, 0.3, query_rows=1)
+    kept = tk[0, :V_full] == 1
+    assert np.allclose(sc[0, kept], 1.0 / (V_b + T), rtol=1e-14)
+    assert np.all(np.isneginf(sc[0, ~kept]))
+    sel = O.select_topk(sc[0], tk[0], V_full, 5)
+    assert sel.tolist() == [0, 1, 2, 3, 4]
+    with pytest.raises(ValueError):
+        oracle.token_scores(q, k, tk, V_full, Hq, Hkv, 0.3, query_rows=0)
+    with pytest.raises(ValueError):
+        oracle.token_scores(q, k, tk, V_full, Hq, Hkv, 0.3, query_rows=T + 1)
 
 
 @pytest.mark.parametrize("seed", range(6))
