@@ -108,6 +108,50 @@ def cpu_baseline(case, r, budget_s=10.0):
                       f"{int(res['cu_seqlens'][-1])} query rows {t_att:.2f} s)"}
 
 
+def clocks_under_load(run_steps, seconds=1.0):
+    """GPU clocks and socket power sampled with amd-smi (a child process) while
+    `run_steps(n)` keeps the GPU busy for about `seconds`; None if amd-smi is
+    unavailable or its output cannot be read."""
+    import shutil
+    import subprocess
+    import threading
+    exe = shutil.which("amd-smi") or "/opt/rocm/bin/amd-smi"
+    if not os.path.exists(exe):
+        return None
+    box = {}
+
+    def sample():
+        time.sleep(0.25 * seconds)
+        try:
+            r = subprocess.run([exe, "metric", "--clock", "--power", "--json"], capture_output=True,
+                               text=True, timeout=20)
+            box["out"] = r.stdout
+        except Exception as e:  # pragma: no cover
+            box["err"] = repr(e)
+
+    th = threading.Thread(target=sample)
+    th.start()
+    t0 = time.perf_counter()
+    while th.is_alive() or time.perf_counter() - t0 < seconds:
+        run_steps(50)
+        if time.perf_counter() - t0 > 30:
+            break
+    th.join(timeout=30)
+    try:
+        txt = box["out"]
+        data = json.loads(txt[txt.index("{"):])
+        g = data["gpu_data"][0] if isinstance(data, dict) else data[0]
+        clk = g.get("clock", {})
+        gfx = [v["clk"]["value"] for k, v in sorted(clk.items()) if k.startswith("gfx") and isinstance(v, dict)
+               and isinstance(v.get("clk"), dict)]
+        mem = clk.get("mem_0", {}).get("clk", {}).get("value") if isinstance(clk.get("mem_0"), dict) else None
+        pw = g.get("power", {}).get("socket_power", {})
+        return {"gfx_mhz": gfx, "mem_mhz": mem, "socket_power_w": pw.get("value") if isinstance(pw, dict) else None,
+                "note": "amd-smi metric --clock --power, sampled while the headline step runs back to back"}
+    except Exception:
+        return None
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -133,7 +177,8 @@ def main():
     class Runner:
         """Preallocated buffers and the three calls of one select + prefill step."""
 
-        def __init__(self, cases):
+        def __init__(self, cases, query_rows=None):
+            self.query_rows = query_rows
             self.sets = [dict(case=c, q=up(c.q, c.dtype), k=up(c.k, c.dtype), v=up(c.v, c.dtype),
                               logit=torch.from_numpy(c.view_logit).to(dev)) for c in cases]
             c = cases[0]
@@ -146,7 +191,7 @@ def main():
                              qc=torch.empty((B * S, Hq, D), dtype=t, device=dev),
                              kc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
                              vc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
-                             workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D),),
+                             workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D, query_rows),),
                                                    dtype=torch.uint8, device=dev))
             self.o = torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device=dev)
 
@@ -158,7 +203,8 @@ def main():
             if ev is not None:
                 ev[1].record(stream)
             lv.token_score_topk(st["q"], st["k"], st["v"], tk, r, c.V_full, q_scale=c.q_scale,
-                                k_scale=c.k_scale, v_scale=c.v_scale, out=self.outs)
+                                k_scale=c.k_scale, v_scale=c.v_scale, out=self.outs,
+                                query_rows=self.query_rows)
             if ev is not None:
                 ev[2].record(stream)
             lv.prefill_attn(self.outs["qc"], self.outs["kc"], self.outs["vc"], self.outs["cu_seqlens"],
@@ -190,6 +236,7 @@ def main():
             torch.cuda.synchronize()
             per = np.array([[e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2]), e[2].elapsed_time(e[3])]
                             for e in evs])
+            self.step_pct = np.percentile(per.sum(axis=1), [10, 50, 90])
             cu = self.outs["cu_seqlens"].cpu().numpy()
             return total_ms / steps, per.mean(axis=0), cu
 
@@ -232,6 +279,7 @@ def main():
     measure = main_runner.measure
 
     ms_step, per, cu = measure(args.keep_ratio, args.steps, args.warmup)
+    step_pct = main_runner.step_pct.copy()
     ms_graph = main_runner.measure_graph(args.keep_ratio, args.steps, args.warmup)
     seqlens = np.diff(cu).tolist()
     fl = attn_flops(seqlens, Hq, D)
@@ -265,11 +313,14 @@ def main():
 
     secondary = []
     if not args.no_sweep:
-        for cfg, name in ((4, "batch 8 ragged (0-4 of 6 views masked per sample), bf16, keep ratio 0.3"),
-                          (5, "batch 8 ragged, fp8 e4m3 Q/K/V with per-tensor scales, bf16 out, keep ratio 0.25")):
-            rn = Runner([synth.config_case(cfg)])
+        for cfg, name, qrows, rr in (
+                (4, "batch 8 ragged (0-4 of 6 views masked per sample), bf16, keep ratio 0.3", None, None),
+                (5, "batch 8 ragged, fp8 e4m3 Q/K/V with per-tensor scales, bf16 out, keep ratio 0.25", None, None),
+                (3, "batch 1, bf16, keep ratio 0.5, scores from the last text token only "
+                    "(litevlm_token_score_topk_rows, 1 query row)", 1, HEADLINE_R)):
+            rn = Runner([synth.config_case(cfg)], query_rows=qrows)
             c = rn.case
-            m, p, cu2 = rn.measure(c.keep_ratio, max(10, args.steps // 2), 3)
+            m, p, cu2 = rn.measure(c.keep_ratio if rr is None else rr, max(10, args.steps // 2), 3)
             sl = np.diff(cu2).tolist()
             f = attn_flops(sl, c.Hq, c.D)
             peak = PEAK_FP8_TFLOPS if c.dtype == "fp8" else PEAK_BF16_TFLOPS
@@ -303,6 +354,9 @@ def main():
                    "global_batch": B, "seq_len": S, "compacted_len": seqlens,
                    "keep_ratio": args.keep_ratio, "parallelism": "none (1 GPU)",
                    "input_sets_rotated": args.sets},
+        "step_ms_p10_p50_p90": {"ms": [round(float(x), 4) for x in step_pct],
+                                "note": "per-step sums of the three calls' event-timed durations "
+                                        "(second pass; event records add small gaps)"},
         "hip_graph": {"ms_per_step": round(ms_graph, 4),
                       "note": "the same steps with each input set's three calls captured in one HIP graph"},
         "prefill_attn_tflops": round(attn_tflops, 1),
@@ -318,6 +372,12 @@ def main():
         "sweep": sweep,
         "secondary": secondary,
     }
+    if not args.no_sweep:
+        def run_steps(n):
+            for i in range(n):
+                main_runner.step(main_runner.sets[i % len(main_runner.sets)], args.keep_ratio)
+            torch.cuda.synchronize()
+        line["gpu_clocks"] = clocks_under_load(run_steps)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(case, args.keep_ratio)
     print(json.dumps(line), flush=True)
