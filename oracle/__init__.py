@@ -21,5 +21,6 @@ from .litevlm import (  # noqa: F401
     compact,
     gather_rows,
     prefill_attention,
+    decode_attention,
     run_path,
 )

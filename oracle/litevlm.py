@@ -246,6 +246,37 @@ def prefill_attention(qc: np.ndarray, kc: np.ndarray, vc: np.ndarray, cu_seqlens
     return out
 
 
+def decode_attention(q1: np.ndarray, k1: np.ndarray, v1: np.ndarray, kc: np.ndarray, vc: np.ndarray,
+                     cu_seqlens: np.ndarray, Hq: int, Hkv: int, scale: float) -> np.ndarray:
+    """Extend-one decode step over the compacted KV cache (Results section:
+    decoding one token after the prefill, where token compression saves little
+    because the work per token is one pass over the cached keys and values).
+    Sample b's new token attends to the S'_b cached tokens of the compacted
+    sequence (packed rows cu_seqlens[b] .. cu_seqlens[b+1] of kc, vc) and to
+    itself, which comes last: o = softmax(q1 . [K; k1]^T * scale) [V; v1], query
+    head h reading KV head h // (Hq/Hkv), softmax in float64 after subtracting
+    the row maximum.
+
+    q1: float64 [B, Hq, D]; k1, v1: float64 [B, Hkv, D]; kc, vc: float64
+    [total, Hkv, D]. Returns float64 [B, Hq, D].
+    """
+    B, _, D = q1.shape
+    G = Hq // Hkv
+    out = np.zeros((B, Hq, v1.shape[2]))
+    for b in range(B):
+        lo, hi = int(cu_seqlens[b]), int(cu_seqlens[b + 1])
+        for h in range(Hq):
+            g = h // G
+            keys = np.concatenate([kc[lo:hi, g, :], k1[b, g][None, :]], axis=0)
+            vals = np.concatenate([vc[lo:hi, g, :], v1[b, g][None, :]], axis=0)
+            logits = (keys @ q1[b, h]) * scale
+            logits -= logits.max()
+            p = np.exp(logits)
+            p /= p.sum()
+            out[b, h] = p @ vals
+    return out
+
+
 # --------------------------------------------------------------------------- whole path
 
 def run_path(case, keep_ratio: Optional[float] = None, attention: bool = True,

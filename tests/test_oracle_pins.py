@@ -549,3 +549,90 @@ def _mutant_attention(kind):
 @pytest.mark.parametrize("kind", ["head_map", "no_scale", "no_causal", "transpose_p"])
 def test_attention_pins_reject_planted_mistakes(kind):
     assert attention_pins(_mutant_attention(kind)) != []
+
+
+# ----------------------------------------------------------------------------- decode (extend one)
+
+def decode_pins(fn, seed=0):
+    """Pins of extend-one decode attention; returns the names of failed pins."""
+    failed = []
+    rng = np.random.default_rng(seed)
+    Hq, Hkv, D = 6, 2, 8
+    G = Hq // Hkv
+    lens = [5, 0, 9, 1]
+    cu = np.concatenate([[0], np.cumsum(lens)]).astype(np.int32)
+    B, tot = len(lens), int(cu[-1])
+    kc = rng.standard_normal((tot, Hkv, D))
+    vc = rng.standard_normal((tot, Hkv, D))
+    q1 = rng.standard_normal((B, Hq, D))
+    k1 = rng.standard_normal((B, Hkv, D))
+    v1 = rng.standard_normal((B, Hkv, D))
+    sc = 1 / math.sqrt(D)
+    got = fn(q1, k1, v1, kc, vc, cu, Hq, Hkv, sc)
+    # torch float64 attention of the one query row over [cache; itself]
+    for b in range(B):
+        lo, hi = cu[b], cu[b + 1]
+        kk = torch.from_numpy(np.concatenate([kc[lo:hi], k1[b][None]], 0).transpose(1, 0, 2).copy())
+        vv = torch.from_numpy(np.concatenate([vc[lo:hi], v1[b][None]], 0).transpose(1, 0, 2).copy())
+        qq = torch.from_numpy(q1[b][:, None, :].copy())
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qq, kk.repeat_interleave(G, 0), vv.repeat_interleave(G, 0), scale=sc)[:, 0].numpy()
+        if not np.allclose(got[b], ref, rtol=1e-12, atol=1e-13):
+            failed.append("sdpa")
+            break
+    # the last row of the prefill attention over the sequence with the new token appended
+    qs, ks, vs, cu2 = [], [], [], [0]
+    for b in range(B):
+        lo, hi = cu[b], cu[b + 1]
+        qs.append(np.concatenate([np.zeros((hi - lo, Hq, D)), q1[b][None]], 0))
+        ks.append(np.concatenate([kc[lo:hi], k1[b][None]], 0))
+        vs.append(np.concatenate([vc[lo:hi], v1[b][None]], 0))
+        cu2.append(cu2[-1] + hi - lo + 1)
+    full = oracle.prefill_attention(np.concatenate(qs), np.concatenate(ks), np.concatenate(vs),
+                                    np.asarray(cu2, np.int32), Hq, Hkv, sc, rows=np.asarray(cu2[1:]) - 1)
+    if not np.allclose(got, full[np.asarray(cu2[1:]) - 1], rtol=1e-12, atol=1e-13):
+        failed.append("prefill_last_row")
+    # Q = 0: the mean of every value row, the new one included
+    gz = fn(np.zeros_like(q1), k1, v1, kc, vc, cu, Hq, Hkv, sc)
+    for b in range(B):
+        lo, hi = cu[b], cu[b + 1]
+        want = np.concatenate([vc[lo:hi], v1[b][None]], 0).mean(0)[np.arange(Hq) // G]
+        if not np.allclose(gz[b], want, rtol=1e-12, atol=1e-14):
+            failed.append("q0_mean")
+            break
+    # an empty cache returns the new value row
+    if not np.allclose(got[1], v1[1][np.arange(Hq) // G], rtol=1e-14):
+        failed.append("empty_cache")
+    return failed
+
+
+def test_decode_pins():
+    for seed in range(3):
+        assert decode_pins(oracle.decode_attention, seed) == []
+
+
+def _mutant_decode(kind):
+    def fn(q1, k1, v1, kc, vc, cu, Hq, Hkv, scale):
+        B, _, D = q1.shape
+        G = Hq // Hkv
+        out = np.zeros((B, Hq, D))
+        for b in range(B):
+            lo, hi = cu[b], cu[b + 1]
+            for h in range(Hq):
+                g = h % Hkv if kind == "head_map" else h // G
+                keys = kc[lo:hi, g] if kind == "no_self" else np.concatenate([kc[lo:hi, g], k1[b, g][None]], 0)
+                vals = vc[lo:hi, g] if kind == "no_self" else np.concatenate([vc[lo:hi, g], v1[b, g][None]], 0)
+                if keys.shape[0] == 0:
+                    continue
+                lg = (keys @ q1[b, h]) * (1.0 if kind == "no_scale" else scale)
+                lg -= lg.max()
+                p = np.exp(lg)
+                p /= p.sum()
+                out[b, h] = p @ vals
+        return out
+    return fn
+
+
+@pytest.mark.parametrize("kind", ["head_map", "no_self", "no_scale"])
+def test_decode_pins_reject_planted_mistakes(kind):
+    assert decode_pins(_mutant_decode(kind)) != []
