@@ -9,6 +9,8 @@
  *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
  *                             (litevlm_token_score_topk_rows: the last n text rows only)
  *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
+ * and, for the token generated after the prefill:
+ *   litevlm_decode_attn       extend-one decode attention over the compacted KV cache
  *
  * Conventions shared by every call
  *   - Pointers marked "dev" are device pointers owned by the caller; the library
@@ -222,6 +224,53 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
                                       const int32_t* cu_seqlens, int32_t max_seqlen,
                                       float softmax_scale, float q_scale, float k_scale,
                                       float v_scale, int32_t causal, void* o, void* stream);
+
+/* Bytes of device workspace litevlm_decode_attn needs for these sizes (0 when
+ * the sizes are invalid or unsupported). */
+size_t litevlm_decode_attn_workspace(int32_t in_dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                     int32_t max_seqlen);
+
+/*
+ * litevlm_decode_attn - extend-one decode attention over the compacted KV cache.
+ *
+ * Paper: Results section (after the prefill, each output token is decoded
+ * against the cached keys and values; the paper measures how little a 3x
+ * token cut saves in this phase, because each decoded token makes one pass
+ * over the cache).
+ *
+ * For each sample b, with the cache rows cu_seqlens[b]..cu_seqlens[b+1]-1 of
+ * kc, vc (n_b = cu_seqlens[b+1]-cu_seqlens[b] rows, the compacted sequence of
+ * the prefill) followed by the new token's own key k1[b] and value v1[b]:
+ *   o[b,h] = v_scale * sum_j softmax_j(l_j) V_j,  l_j = q1[b,h] . K_j * softmax_scale*q_scale*k_scale,
+ *   j over the n_b cached tokens and the new token (which comes last and sees
+ *   everything before it, so no mask applies); query head h reads KV head h/G.
+ *   Softmax and accumulation in fp32.
+ *
+ *   in_dtype           LITEVLM_F32, LITEVLM_BF16 or LITEVLM_FP8_E4M3 (q1, k1, v1, kc, vc)
+ *   out_dtype          LITEVLM_F32 or LITEVLM_BF16
+ *   B, Hq, Hkv, D      batch, heads (G = Hq/Hkv in {1, 2, 4, 8}, else
+ *                      LITEVLM_ERR_UNSUPPORTED), head dim (64 or 128)
+ *   q1                 dev [B, Hq, D]: the new token's queries
+ *   k1, v1             dev [B, Hkv, D]: the new token's key and value
+ *   kc, vc             dev [total, Hkv, D], total = cu_seqlens[B]: the compacted cache
+ *                      (the kc, vc of litevlm_token_score_topk)
+ *   cu_seqlens         dev int32 [B+1], non-decreasing, cu_seqlens[0] = 0
+ *   max_seqlen         host upper bound on every n_b; the split grid is sized from it
+ *                      and surplus splits exit at once. Longer segments give
+ *                      undefined values (no out-of-range access).
+ *   softmax_scale, q_scale, k_scale, v_scale   finite, > 0; scales must be 1 unless FP8
+ *   o                  dev out [B, Hq, D] in out_dtype
+ *   workspace          dev scratch of litevlm_decode_attn_workspace() bytes (partial
+ *                      results of the key splits); contents on entry are ignored, and
+ *                      calls that may run concurrently must not share one workspace
+ */
+litevlm_status_t litevlm_decode_attn(int32_t in_dtype, int32_t out_dtype, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t D, const void* q1, const void* k1,
+                                     const void* v1, const void* kc, const void* vc,
+                                     const int32_t* cu_seqlens, int32_t max_seqlen,
+                                     float softmax_scale, float q_scale, float k_scale,
+                                     float v_scale, void* o, void* workspace,
+                                     size_t workspace_bytes, void* stream);
 
 #ifdef __cplusplus
 }

@@ -8,6 +8,7 @@ the path runs in the library's HIP kernels:
     patch_select(...)      view selection and per-view patch masking
     token_score_topk(...)  visual-token scoring, top-k and gather compaction
     prefill_attn(...)      causal GQA prefill attention over the packed sequence
+    decode_attn(...)       extend-one decode attention over the compacted KV cache
 """
 from __future__ import annotations
 
@@ -20,8 +21,8 @@ import torch
 from . import _abi
 from ._abi import LiteVLMError, load  # noqa: F401
 
-__all__ = ["patch_select", "token_score_topk", "prefill_attn", "dtype_code", "workspace_bytes",
-           "LiteVLMError", "load"]
+__all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "dtype_code",
+           "workspace_bytes", "decode_workspace_bytes", "LiteVLMError", "load"]
 
 
 def dtype_code(t: torch.dtype) -> int:
@@ -143,4 +144,38 @@ def prefill_attn(qc: torch.Tensor, kc: torch.Tensor, vc: torch.Tensor, cu_seqlen
         _ptr(cu_seqlens), int(max_seqlen), float(softmax_scale), float(q_scale), float(k_scale),
         float(v_scale), 1 if causal else 0, _ptr(o), _stream(qc.device))
     _abi.check(st, "litevlm_prefill_attn")
+    return o
+
+
+def decode_workspace_bytes(in_dtype: torch.dtype, B: int, Hq: int, Hkv: int, D: int,
+                           max_seqlen: int) -> int:
+    return int(load().litevlm_decode_attn_workspace(dtype_code(in_dtype), B, Hq, Hkv, D, int(max_seqlen)))
+
+
+def decode_attn(q1: torch.Tensor, k1: torch.Tensor, v1: torch.Tensor, kc: torch.Tensor,
+                vc: torch.Tensor, cu_seqlens: torch.Tensor, max_seqlen: int,
+                softmax_scale: Optional[float] = None, q_scale: float = 1.0, k_scale: float = 1.0,
+                v_scale: float = 1.0, out_dtype: Optional[torch.dtype] = None,
+                out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """One decode step per sample over the compacted cache. q1: [B,Hq,D], k1/v1:
+    [B,Hkv,D] (the new token), kc/vc: [rows,Hkv,D] with rows >= cu_seqlens[B].
+    Returns [B,Hq,D] in out_dtype (bf16 by default, fp32 for fp32 input)."""
+    lib = load()
+    B, Hq, D = q1.shape
+    Hkv = k1.shape[1]
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    if out_dtype is None:
+        out_dtype = torch.float32 if q1.dtype == torch.float32 else torch.bfloat16
+    o = out if out is not None else torch.empty((B, Hq, D), dtype=out_dtype, device=q1.device)
+    nbytes = decode_workspace_bytes(q1.dtype, B, Hq, Hkv, D, max_seqlen)
+    ws = workspace if workspace is not None else torch.empty((max(nbytes, 1),), dtype=torch.uint8,
+                                                             device=q1.device)
+    st = lib.litevlm_decode_attn(
+        dtype_code(q1.dtype), dtype_code(o.dtype), B, Hq, Hkv, D, _ptr(q1), _ptr(k1), _ptr(v1),
+        _ptr(kc), _ptr(vc), _ptr(cu_seqlens), int(max_seqlen), float(softmax_scale), float(q_scale),
+        float(k_scale), float(v_scale), _ptr(o), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(q1.device))
+    _abi.check(st, "litevlm_decode_attn")
     return o

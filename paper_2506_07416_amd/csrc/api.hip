@@ -29,6 +29,22 @@ litevlm_status_t check_score_shape(int32_t B, int32_t S, int32_t V_full, int32_t
   return LITEVLM_OK;
 }
 
+// Decode: G = Hq/Hkv query heads per KV head must be 1, 2, 4 or 8 (the kernel
+// holds every query head of a KV head in registers).
+litevlm_status_t check_decode_shape(int32_t in_dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                    int32_t max_seqlen) {
+  if (!valid_dtype(in_dtype)) return LITEVLM_ERR_UNSUPPORTED;
+  if (B < 1 || B > LITEVLM_MAX_BATCH || Hq < 1 || Hkv < 1 || Hq % Hkv != 0 ||
+      Hq > LITEVLM_MAX_HEADS || (D != 64 && D != 128) || max_seqlen < 0)
+    return LITEVLM_ERR_BAD_SHAPE;
+  if ((int64_t)B * (max_seqlen + 1) > INT32_MAX / 2) return LITEVLM_ERR_BAD_SHAPE;
+  // the split grid (at most B*Hkv*((max_seqlen+64)/64) workgroups) must fit an int
+  if ((int64_t)B * Hkv * ((max_seqlen + 64) / 64) > INT32_MAX) return LITEVLM_ERR_BAD_SHAPE;
+  const int G = Hq / Hkv;
+  if (G != 1 && G != 2 && G != 4 && G != 8) return LITEVLM_ERR_UNSUPPORTED;
+  return LITEVLM_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -192,6 +208,57 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
   a.out_scale = v_scale;
   a.o = o;
   return hip_status(launch_prefill_attn(a, static_cast<hipStream_t>(stream)));
+}
+
+size_t litevlm_decode_attn_workspace(int32_t in_dtype, int32_t B, int32_t Hq, int32_t Hkv, int32_t D,
+                                     int32_t max_seqlen) {
+  if (check_decode_shape(in_dtype, B, Hq, Hkv, D, max_seqlen) != LITEVLM_OK) return 0;
+  return decode_layout(in_dtype, B, Hq, Hkv, D, max_seqlen).total;
+}
+
+litevlm_status_t litevlm_decode_attn(int32_t in_dtype, int32_t out_dtype, int32_t B, int32_t Hq,
+                                     int32_t Hkv, int32_t D, const void* q1, const void* k1,
+                                     const void* v1, const void* kc, const void* vc,
+                                     const int32_t* cu_seqlens, int32_t max_seqlen,
+                                     float softmax_scale, float q_scale, float k_scale,
+                                     float v_scale, void* o, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  if (!q1 || !k1 || !v1 || !kc || !vc || !cu_seqlens || !o) return LITEVLM_ERR_NULL_POINTER;
+  if (!valid_dtype(in_dtype) || (out_dtype != LITEVLM_F32 && out_dtype != LITEVLM_BF16))
+    return LITEVLM_ERR_UNSUPPORTED;
+  const litevlm_status_t sh = check_decode_shape(in_dtype, B, Hq, Hkv, D, max_seqlen);
+  if (sh != LITEVLM_OK) return sh;
+  if (!finite_pos(softmax_scale) || !finite_pos(q_scale) || !finite_pos(k_scale) ||
+      !finite_pos(v_scale))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (in_dtype != LITEVLM_FP8_E4M3 && (q_scale != 1.f || k_scale != 1.f || v_scale != 1.f))
+    return LITEVLM_ERR_BAD_VALUE;
+  const void* big[] = {q1, k1, v1, kc, vc, o, workspace};
+  for (const void* p : big)
+    if (p && !aligned(p, 16)) return LITEVLM_ERR_MISALIGNED;
+  if (!aligned(cu_seqlens, 4)) return LITEVLM_ERR_MISALIGNED;
+  const size_t need = decode_layout(in_dtype, B, Hq, Hkv, D, max_seqlen).total;
+  if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
+
+  DecodeArgs a;
+  a.in_dtype = in_dtype;
+  a.out_dtype = out_dtype;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.max_seqlen = max_seqlen;
+  a.q1 = q1;
+  a.k1 = k1;
+  a.v1 = v1;
+  a.kc = kc;
+  a.vc = vc;
+  a.cu_seqlens = cu_seqlens;
+  a.logit_scale_log2 = (float)((double)softmax_scale * q_scale * k_scale * 1.4426950408889634);
+  a.out_scale = v_scale;
+  a.o = o;
+  a.workspace = workspace;
+  return hip_status(launch_decode_attn(a, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -59,4 +59,28 @@ struct AttnArgs {
 };
 hipError_t launch_prefill_attn(const AttnArgs& a, hipStream_t stream);
 
+// Workspace of the decode step: per (sample, query head, key split) the
+// unnormalised output float [D] and the split's (max, sum) float2. The split
+// length and count follow from the shape and the host bound max_seqlen.
+struct DecodeLayout {
+  int split_len, nsplit;
+  size_t part_o_off, part_ml_off, total;
+};
+DecodeLayout decode_layout(int in_dtype, int B, int Hq, int Hkv, int D, int max_seqlen);
+
+struct DecodeArgs {
+  int in_dtype, out_dtype, B, Hq, Hkv, D, max_seqlen;
+  const void* q1;
+  const void* k1;
+  const void* v1;
+  const void* kc;
+  const void* vc;
+  const int32_t* cu_seqlens;
+  float logit_scale_log2;  // softmax_scale*q_scale*k_scale*log2(e)
+  float out_scale;         // v_scale
+  void* o;
+  void* workspace;
+};
+hipError_t launch_decode_attn(const DecodeArgs& a, hipStream_t stream);
+
 }  // namespace litevlm

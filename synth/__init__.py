@@ -207,3 +207,31 @@ def random_attention_inputs(seqlens: Sequence[int], Hq: int, Hkv: int, D: int, d
     kb, ks = encode(k, dtype)
     vb, vsc = encode(v, dtype)
     return qb, kb, vb, (qs, ks, vsc), cu
+
+
+def encode_with_scale(x: np.ndarray, dtype: str, scale: float) -> np.ndarray:
+    """Stored bits of ``x`` under a given per-tensor scale (fp8: clamp x/scale to
+    +-448 and round to nearest even; other dtypes ignore the scale, which is 1)."""
+    if dtype != FP8:
+        return encode(x, dtype)[0]
+    y = np.clip(x / np.float32(scale), -E4M3_MAX, E4M3_MAX).astype(np.float32)
+    return torch.from_numpy(np.ascontiguousarray(y)).to(torch.float8_e4m3fn).view(torch.uint8).numpy().copy()
+
+
+def decode_token_inputs(B: int, Hq: int, Hkv: int, D: int, dtype: str, seed: int,
+                        scales: Optional[Sequence[float]] = None, peaked: bool = False):
+    """The query, key and value of one new token per sample for a decode step
+    after the prefill: q1 ``[B,Hq,D]``, k1/v1 ``[B,Hkv,D]`` from the same
+    distribution as the prompt (N(0,1)/sqrt(D); Q and K unscaled when peaked).
+    For fp8, ``scales`` = (q, k, v) scales of the cache the token joins; without
+    them each tensor gets its own amax/448 scale. Returns (q1, k1, v1, scales)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    div = np.float32(1.0 if peaked else np.sqrt(D))
+    q = rng.standard_normal((B, Hq, D), dtype=np.float32) / div
+    k = rng.standard_normal((B, Hkv, D), dtype=np.float32) / div
+    v = rng.standard_normal((B, Hkv, D), dtype=np.float32) / np.float32(np.sqrt(D))
+    if scales is None:
+        (qb, qs), (kb, ks), (vb, vs) = encode(q, dtype), encode(k, dtype), encode(v, dtype)
+        return qb, kb, vb, (qs, ks, vs)
+    return (encode_with_scale(q, dtype, scales[0]), encode_with_scale(k, dtype, scales[1]),
+            encode_with_scale(v, dtype, scales[2]), tuple(float(s) for s in scales))

@@ -176,3 +176,54 @@ def test_binding_fails_loudly_without_library(monkeypatch, tmp_path):
     monkeypatch.setattr(_abi, "LIB_PATH", str(tmp_path / "missing.so"))
     with pytest.raises(ImportError):
         _abi.load()
+
+
+# ----------------------------------------------------------------------------- decode_attn
+
+def da(ind=_abi.BF16, outd=_abi.BF16, B=2, Hq=32, Hkv=8, D=128, q1=A, k1=A, v1=A, kc=A, vc=A, cu=A,
+       ml=3200, sm=0.088, qs=1.0, ks=1.0, vs=1.0, o=A, ws=A, wsb=None):
+    lib = lv.load()
+    if wsb is None:
+        wsb = lib.litevlm_decode_attn_workspace(ind, B, Hq, Hkv, D, ml)
+    return lib.litevlm_decode_attn(ind, outd, B, Hq, Hkv, D, q1, k1, v1, kc, vc, cu, ml, sm, qs, ks,
+                                   vs, o, ws, wsb, None)
+
+
+def test_decode_workspace_size():
+    lib = lv.load()
+    # batch 1, 8 KV heads: short splits (64 keys) so the grid fills the chip
+    n = lib.litevlm_decode_attn_workspace(_abi.BF16, 1, 32, 8, 128, 3200)
+    splits = (3200 + 64) // 64
+    assert n >= 32 * splits * (128 * 4 + 8)
+    # batch 8: long splits (256 keys) already give enough workgroups
+    n8 = lib.litevlm_decode_attn_workspace(_abi.BF16, 8, 32, 8, 128, 6272)
+    assert 8 * 32 * ((6272 + 256) // 256) * (128 * 4 + 8) <= n8 < 8 * 32 * ((6272 + 64) // 64) * 520
+    assert lib.litevlm_decode_attn_workspace(_abi.BF16, 1, 32, 8, 128, 0) > 0   # new token only
+    assert lib.litevlm_decode_attn_workspace(_abi.BF16, 1, 48, 8, 128, 100) == 0  # G = 6
+    assert lib.litevlm_decode_attn_workspace(_abi.BF16, 1, 32, 3, 128, 100) == 0  # Hq % Hkv
+    assert lib.litevlm_decode_attn_workspace(9, 1, 32, 8, 128, 100) == 0
+
+
+def test_decode_attn_validation():
+    assert da(q1=None) == _abi.ERR_NULL_POINTER
+    assert da(k1=None) == _abi.ERR_NULL_POINTER
+    assert da(vc=None) == _abi.ERR_NULL_POINTER
+    assert da(cu=None) == _abi.ERR_NULL_POINTER
+    assert da(o=None) == _abi.ERR_NULL_POINTER
+    assert da(ind=5, wsb=1 << 20) == _abi.ERR_UNSUPPORTED
+    assert da(outd=_abi.FP8_E4M3) == _abi.ERR_UNSUPPORTED
+    assert da(Hq=48, wsb=1 << 20) == _abi.ERR_UNSUPPORTED       # G = 6
+    assert da(Hq=256, Hkv=16, wsb=1 << 20) == _abi.ERR_BAD_SHAPE
+    assert da(Hkv=3, wsb=1 << 20) == _abi.ERR_BAD_SHAPE
+    assert da(D=96, wsb=1 << 20) == _abi.ERR_BAD_SHAPE
+    assert da(B=0, wsb=1 << 20) == _abi.ERR_BAD_SHAPE
+    assert da(ml=-1, wsb=1 << 20) == _abi.ERR_BAD_SHAPE
+    assert da(sm=0.0) == _abi.ERR_BAD_VALUE
+    assert da(qs=2.0) == _abi.ERR_BAD_VALUE                    # scales only for fp8
+    assert da(ind=_abi.FP8_E4M3, vs=float("nan")) == _abi.ERR_BAD_VALUE
+    assert da(kc=MIS) == _abi.ERR_MISALIGNED
+    assert da(o=MIS) == _abi.ERR_MISALIGNED
+    assert da(ws=MIS) == _abi.ERR_MISALIGNED
+    assert da(cu=A + 2) == _abi.ERR_MISALIGNED
+    assert da(ws=None) == _abi.ERR_WORKSPACE
+    assert da(wsb=64) == _abi.ERR_WORKSPACE
