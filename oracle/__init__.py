@@ -24,3 +24,4 @@ from .litevlm import (  # noqa: F401
     decode_attention,
     run_path,
 )
+from . import tsm  # noqa: F401,E402  (the Token Selection Module front end)
