@@ -331,6 +331,44 @@ def main():
                 "frac_hbm": round(moved / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                 "copies_rotated": ncopy, "timing": "HIP graph of one call per cache copy, replayed"}
 
+    def measure_tsm(cfg, label, iters=20, warmup=3):
+        """The Token Selection Module front end (litevlm_tsm_qk) on the workload's
+        shape with model width Hq*D: scoring keys for every token and queries for
+        the text tokens from seeded bf16 hidden states, positions from the
+        workload's patch selection. Events around `iters` back-to-back calls."""
+        c = synth.config_case(cfg)
+        Dm = c.Hq * c.D
+        hid, gamma, wq, wk = synth.tsm_inputs(c.B, c.S, Dm, c.Hq, c.Hkv, c.D, seed=31)
+        x = up(hid, "bf16")
+        g = torch.from_numpy(gamma).to(dev)
+        wq_f = lv.tsm_fold_gain(up(wq, "bf16"), g)
+        wk_f = lv.tsm_fold_gain(up(wk, "bf16"), g)
+        _, tk, nv = lv.patch_select(torch.from_numpy(c.view_logit).to(dev), c.view_offsets, c.S, c.w_lexical,
+                                    c.threshold)
+        q = torch.empty((c.B, c.S, c.Hq, c.D), dtype=torch.bfloat16, device=dev)
+        k = torch.empty((c.B, c.S, c.Hkv, c.D), dtype=torch.bfloat16, device=dev)
+        for _ in range(warmup):
+            lv.tsm_qk(x, tk, c.V_full, wq_f, wk_f, c.Hq, c.Hkv, c.D, q=q, k=k)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(iters):
+            lv.tsm_qk(x, tk, c.V_full, wq_f, wk_f, c.Hq, c.Hkv, c.D, q=q, k=k)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        us = t0.elapsed_time(t1) / iters * 1e3
+        T = c.S - c.V_full
+        kept = int(nv.sum().item()) + c.B * T
+        fl_alg = 2.0 * Dm * (kept * c.Hkv * c.D + c.B * T * c.Hq * c.D)
+        fl_done = 2.0 * Dm * (c.B * c.S * c.Hkv * c.D + c.B * T * c.Hq * c.D)
+        return {"workload": label, "model_width": Dm, "tsm_us": round(us, 2),
+                "gflop_algorithmic": round(fl_alg / 1e9, 2), "gflop_computed": round(fl_done / 1e9, 2),
+                "tflops": round(fl_alg / (us * 1e-6) / 1e12, 1),
+                "frac_bf16_peak": round(fl_alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                "note": "keys of the kept tokens and queries of the text tokens count as algorithmic; "
+                        "the kernel also projects the keys of dropped views' tokens"}
+
     if args.workload == 3:
         main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])
     else:
@@ -374,8 +412,11 @@ def main():
                           "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                           "attn_frac_bf16_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
 
-    secondary, decode_lines = [], []
+    secondary, decode_lines, tsm_lines = [], [], []
     if not args.no_sweep:
+        tsm_lines.append(measure_tsm(3, "6 views x 1024 + 128 text, batch 1, GQA 32/8, D=128, model width 4096"))
+        tsm_lines.append(measure_tsm(4, "batch 8 ragged (0-4 of 6 views dropped per sample), same shape"))
+        torch.cuda.empty_cache()
         decode_lines.append(measure_decode(main_runner, args.keep_ratio,
                                            "decode step after the prefill: the headline workload"))
         for cfg, name, qrows, rr in (
@@ -440,6 +481,7 @@ def main():
         "sweep": sweep,
         "secondary": secondary,
         "decode": decode_lines,
+        "tsm_front_end": tsm_lines,
     }
     if not args.no_sweep:
         def run_steps(n):

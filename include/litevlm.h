@@ -9,6 +9,9 @@
  *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
  *                             (litevlm_token_score_topk_rows: the last n text rows only)
  *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
+ * in front of the scoring, from the hidden states:
+ *   litevlm_tsm_qk            the Token Selection Module's scoring queries and keys
+ *                             (litevlm_tsm_fold_gain prepares its weights)
  * and, for the token generated after the prefill:
  *   litevlm_decode_attn       extend-one decode attention over the compacted KV cache
  *
@@ -224,6 +227,53 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
                                       const int32_t* cu_seqlens, int32_t max_seqlen,
                                       float softmax_scale, float q_scale, float k_scale,
                                       float v_scale, int32_t causal, void* o, void* stream);
+
+/*
+ * litevlm_tsm_qk - the Token Selection Module's scoring queries and keys from
+ * the hidden states entering its decoder layer.
+ *
+ * Paper: Design section, Token Selection Module paragraph (the first decoder
+ * layer of the finetuned LLM, run standalone, scores the visual tokens);
+ * Experiments section (the decoder is InternLM2.5). The layer's attention takes
+ * its queries and keys from RMS-normalised hidden states through bias-free
+ * projections and rotary position embeddings:
+ *   r_j      = 1 / sqrt(mean_c x[b,j,c]^2 + eps)
+ *   k[b,j,h] = rope(r_j * (x[b,j] . W_k'[h*D:(h+1)*D]), pos_j)   for every token j
+ *   q[b,t,h] = rope(r_t * (x[b,t] . W_q'[h*D:(h+1)*D]), pos_t)   for the text tokens t
+ *   rope pairs element d < D/2 of a head with element d + D/2 and rotates the
+ *   pair by the angle pos * rope_theta^(-2d/D);
+ *   pos_j = the number of kept tokens before j (its position in the
+ *   patch-selected sequence; token_keep NULL: pos_j = j).
+ * Products in bf16 on MFMA with fp32 accumulation; the outputs are rounded to
+ * bf16. The results are the q and k that litevlm_token_score_topk reads.
+ *
+ *   B, S, V_full       batch, sequence length, visual tokens (T = S - V_full >= 1)
+ *   Dm                 model width: a multiple of 32, at most 65536
+ *   Hq, Hkv, D         heads (Hq % Hkv == 0), head dim 64 or 128; Hq*D and Hkv*D must
+ *                      be multiples of 128 (else LITEVLM_ERR_UNSUPPORTED)
+ *   hidden             dev bf16 [B, S, Dm]
+ *   token_keep         dev uint8 [B, S] from litevlm_patch_select, or NULL
+ *   w_q, w_k           dev bf16 [Hq*D, Dm], [Hkv*D, Dm]: the projections with the RMS
+ *                      normalisation gain folded in (litevlm_tsm_fold_gain)
+ *   eps                RMS normalisation epsilon (finite, > 0)
+ *   rope_theta         rotary base (finite, > 1)
+ *   q                  dev out bf16 [B, S, Hq, D]: rows V_full..S-1 of every sample are
+ *                      written, the visual rows are left untouched
+ *   k                  dev out bf16 [B, S, Hkv, D]: every row written
+ */
+litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm, int32_t Hq, int32_t Hkv,
+                                int32_t D, const void* hidden, const uint8_t* token_keep, const void* w_q,
+                                const void* w_k, float eps, float rope_theta, void* q, void* k,
+                                void* stream);
+
+/*
+ * litevlm_tsm_fold_gain - w_out[n, c] = bf16(w[n, c] * gamma[c]): folds the RMS
+ * normalisation gain into the projection that follows it, once per set of
+ * weights (the form litevlm_tsm_qk takes). w and w_out are dev bf16
+ * [rows, cols] (may be the same buffer), gamma dev fp32 [cols].
+ */
+litevlm_status_t litevlm_tsm_fold_gain(int32_t rows, int32_t cols, const void* w, const float* gamma,
+                                       void* w_out, void* stream);
 
 /* Bytes of device workspace litevlm_decode_attn needs for these sizes (0 when
  * the sizes are invalid or unsupported). */

@@ -9,6 +9,7 @@ the path runs in the library's HIP kernels:
     token_score_topk(...)  visual-token scoring, top-k and gather compaction
     prefill_attn(...)      causal GQA prefill attention over the packed sequence
     decode_attn(...)       extend-one decode attention over the compacted KV cache
+    tsm_qk(...)            the Token Selection Module's scoring q and k from hidden states
 """
 from __future__ import annotations
 
@@ -21,7 +22,8 @@ import torch
 from . import _abi
 from ._abi import LiteVLMError, load  # noqa: F401
 
-__all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "dtype_code",
+__all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "tsm_qk", "tsm_fold_gain",
+           "dtype_code",
            "workspace_bytes", "decode_workspace_bytes", "LiteVLMError", "load"]
 
 
@@ -179,3 +181,28 @@ def decode_attn(q1: torch.Tensor, k1: torch.Tensor, v1: torch.Tensor, kc: torch.
         _stream(q1.device))
     _abi.check(st, "litevlm_decode_attn")
     return o
+
+
+def tsm_fold_gain(w: torch.Tensor, gamma: torch.Tensor, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """bf16 w [rows, cols] times the fp32 gain gamma [cols] per column, rounded to bf16."""
+    rows, cols = w.shape
+    o = out if out is not None else torch.empty_like(w)
+    st = load().litevlm_tsm_fold_gain(rows, cols, _ptr(w), _ptr(gamma), _ptr(o), _stream(w.device))
+    _abi.check(st, "litevlm_tsm_fold_gain")
+    return o
+
+
+def tsm_qk(hidden: torch.Tensor, token_keep: Optional[torch.Tensor], V_full: int, w_q: torch.Tensor,
+           w_k: torch.Tensor, Hq: int, Hkv: int, D: int, eps: float = 1e-5, rope_theta: float = 1e6,
+           q: Optional[torch.Tensor] = None, k: Optional[torch.Tensor] = None):
+    """Scoring queries (text rows) and keys (all rows) of the Token Selection
+    Module from bf16 hidden states [B,S,Dm]; w_q/w_k carry the folded RMS gain.
+    Returns (q [B,S,Hq,D], k [B,S,Hkv,D]) in bf16; q's visual rows are untouched."""
+    B, S, Dm = hidden.shape
+    dev = hidden.device
+    q = q if q is not None else torch.empty((B, S, Hq, D), dtype=torch.bfloat16, device=dev)
+    k = k if k is not None else torch.empty((B, S, Hkv, D), dtype=torch.bfloat16, device=dev)
+    st = load().litevlm_tsm_qk(B, S, V_full, Dm, Hq, Hkv, D, _ptr(hidden), _ptr(token_keep), _ptr(w_q),
+                               _ptr(w_k), float(eps), float(rope_theta), _ptr(q), _ptr(k), _stream(dev))
+    _abi.check(st, "litevlm_tsm_qk")
+    return q, k

@@ -261,4 +261,47 @@ litevlm_status_t litevlm_decode_attn(int32_t in_dtype, int32_t out_dtype, int32_
   return hip_status(launch_decode_attn(a, static_cast<hipStream_t>(stream)));
 }
 
+litevlm_status_t litevlm_tsm_fold_gain(int32_t rows, int32_t cols, const void* w, const float* gamma,
+                                       void* w_out, void* stream) {
+  if (!w || !gamma || !w_out) return LITEVLM_ERR_NULL_POINTER;
+  if (rows < 1 || cols < 1 || (int64_t)rows * cols > ((int64_t)1 << 40)) return LITEVLM_ERR_BAD_SHAPE;
+  if (!aligned(w, 2) || !aligned(w_out, 2) || !aligned(gamma, 4)) return LITEVLM_ERR_MISALIGNED;
+  return hip_status(launch_tsm_fold_gain(w, gamma, w_out, rows, cols, static_cast<hipStream_t>(stream)));
+}
+
+litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm, int32_t Hq, int32_t Hkv,
+                                int32_t D, const void* hidden, const uint8_t* token_keep, const void* w_q,
+                                const void* w_k, float eps, float rope_theta, void* q, void* k,
+                                void* stream) {
+  if (!hidden || !w_q || !w_k || !q || !k) return LITEVLM_ERR_NULL_POINTER;
+  if (B < 1 || B > LITEVLM_MAX_BATCH || V_full < 0 || S <= V_full || Hq < 1 || Hkv < 1 ||
+      Hq > LITEVLM_MAX_HEADS || Hq % Hkv != 0 || (D != 64 && D != 128))
+    return LITEVLM_ERR_BAD_SHAPE;
+  if (Dm < 32 || Dm % 32 != 0 || Dm > 65536) return LITEVLM_ERR_BAD_SHAPE;
+  // a workgroup covers 128 output features: whole heads, rotary partners together
+  if ((Hq * D) % 128 != 0 || (Hkv * D) % 128 != 0) return LITEVLM_ERR_UNSUPPORTED;
+  if ((int64_t)B * S > INT32_MAX / 2 || (int64_t)B * S * Dm > ((int64_t)1 << 40)) return LITEVLM_ERR_BAD_SHAPE;
+  if (!(eps > 0.f) || !isfinite(eps) || !(rope_theta > 1.f) || !isfinite(rope_theta))
+    return LITEVLM_ERR_BAD_VALUE;
+  if (!aligned(hidden, 16) || !aligned(w_q, 16) || !aligned(w_k, 16) || !aligned(q, 16) || !aligned(k, 16))
+    return LITEVLM_ERR_MISALIGNED;
+  TsmArgs a;
+  a.B = B;
+  a.S = S;
+  a.V_full = V_full;
+  a.Dm = Dm;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.D = D;
+  a.hidden = hidden;
+  a.token_keep = token_keep;
+  a.w_q = w_q;
+  a.w_k = w_k;
+  a.eps = eps;
+  a.rope_theta = rope_theta;
+  a.q = q;
+  a.k = k;
+  return hip_status(launch_tsm_qk(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

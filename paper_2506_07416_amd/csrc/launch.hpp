@@ -83,4 +83,18 @@ struct DecodeArgs {
 };
 hipError_t launch_decode_attn(const DecodeArgs& a, hipStream_t stream);
 
+struct TsmArgs {
+  int B, S, V_full, Dm, Hq, Hkv, D;
+  const void* hidden;
+  const uint8_t* token_keep;
+  const void* w_q;
+  const void* w_k;
+  float eps, rope_theta;
+  void* q;
+  void* k;
+};
+hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream);
+hipError_t launch_tsm_fold_gain(const void* w, const float* gamma, void* w_out, int rows, int cols,
+                                hipStream_t stream);
+
 }  // namespace litevlm

@@ -235,3 +235,16 @@ def decode_token_inputs(B: int, Hq: int, Hkv: int, D: int, dtype: str, seed: int
         return qb, kb, vb, (qs, ks, vs)
     return (encode_with_scale(q, dtype, scales[0]), encode_with_scale(k, dtype, scales[1]),
             encode_with_scale(v, dtype, scales[2]), tuple(float(s) for s in scales))
+
+
+def tsm_inputs(B: int, S: int, Dm: int, Hq: int, Hkv: int, D: int, seed: int):
+    """Inputs of the Token Selection Module front end: hidden states [B,S,Dm]
+    from N(0,1), an RMS gain [Dm] from 1 + 0.1*N(0,1) (fp32), and projection
+    weights w_q [Hq*D, Dm], w_k [Hkv*D, Dm] from N(0, 1/Dm), the bf16 ones as
+    round-to-nearest-even bits. Returns (hidden, gamma, w_q, w_k)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    hidden = rng.standard_normal((B, S, Dm), dtype=np.float32)
+    gamma = (1.0 + 0.1 * rng.standard_normal(Dm)).astype(np.float32)
+    w_q = rng.standard_normal((Hq * D, Dm), dtype=np.float32) / np.float32(np.sqrt(Dm))
+    w_k = rng.standard_normal((Hkv * D, Dm), dtype=np.float32) / np.float32(np.sqrt(Dm))
+    return _to_bf16_bits(hidden), gamma, _to_bf16_bits(w_q), _to_bf16_bits(w_k)

@@ -227,3 +227,26 @@ def test_decode_attn_validation():
     assert da(cu=A + 2) == _abi.ERR_MISALIGNED
     assert da(ws=None) == _abi.ERR_WORKSPACE
     assert da(wsb=64) == _abi.ERR_WORKSPACE
+
+
+def test_tsm_validation():
+    lib = lv.load()
+
+    def tq(B=1, S=100, V=80, Dm=256, Hq=8, Hkv=2, D=128, x=A, keep=A, wq=A, wk=A, eps=1e-5, th=1e6, q=A, k=A):
+        return lib.litevlm_tsm_qk(B, S, V, Dm, Hq, Hkv, D, x, keep, wq, wk, eps, th, q, k, None)
+    assert tq(x=None) == _abi.ERR_NULL_POINTER
+    assert tq(wk=None) == _abi.ERR_NULL_POINTER
+    assert tq(q=None) == _abi.ERR_NULL_POINTER
+    assert tq(S=80) == _abi.ERR_BAD_SHAPE                     # no text token
+    assert tq(Dm=100) == _abi.ERR_BAD_SHAPE                   # not a multiple of 32
+    assert tq(D=96) == _abi.ERR_BAD_SHAPE
+    assert tq(Hkv=3) == _abi.ERR_BAD_SHAPE
+    assert tq(Hq=2, Hkv=1, D=64) == _abi.ERR_UNSUPPORTED       # Hkv*D = 64 < 128
+    assert tq(eps=0.0) == _abi.ERR_BAD_VALUE
+    assert tq(th=1.0) == _abi.ERR_BAD_VALUE
+    assert tq(th=float("inf")) == _abi.ERR_BAD_VALUE
+    assert tq(x=MIS) == _abi.ERR_MISALIGNED
+    assert tq(k=MIS) == _abi.ERR_MISALIGNED
+    assert lib.litevlm_tsm_fold_gain(4, 8, None, A, A, None) == _abi.ERR_NULL_POINTER
+    assert lib.litevlm_tsm_fold_gain(0, 8, A, A, A, None) == _abi.ERR_BAD_SHAPE
+    assert lib.litevlm_tsm_fold_gain(4, 8, A, A + 2, A, None) == _abi.ERR_MISALIGNED

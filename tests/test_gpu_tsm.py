@@ -1,0 +1,89 @@
+"""GPU parity of the Token Selection Module front end (litevlm_tsm_qk, with
+the gain folded by litevlm_tsm_fold_gain) against the oracle's tsm_qk.
+
+The oracle takes the gain and the unfolded weights in float64; the GPU folds
+the gain into bf16 weights and rounds its outputs to bf16, so the comparison
+allows for bf16 rounding: |got - ref| <= 1e-2 + 2e-2*|ref| elementwise and a
+per-(row, head) relative L2 error of at most 1e-2 (bf16 output rounding alone
+gives about 2e-3, the folded-weight rounding about as much again)."""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2506_07416_amd as lv
+import synth
+from oracle import tsm as OT
+from parity_util import log, row_rel_l2, to_device, to_float64
+
+pytestmark = pytest.mark.gpu
+
+EPS, THETA = 1e-5, 1e6
+TSM_RTOL, TSM_ATOL, TSM_ROW_L2 = 2e-2, 1e-2, 1e-2
+
+
+def run(case, Dm, seed, eps=EPS, theta=THETA, use_keep=True):
+    B, S, V, Hq, Hkv, D = case.B, case.S, case.V_full, case.Hq, case.Hkv, case.D
+    hid, gamma, wq, wk = synth.tsm_inputs(B, S, Dm, Hq, Hkv, D, seed)
+    tk = None
+    keep_ref = np.ones((B, S), np.uint8)
+    if use_keep:
+        _, tk, _ = lv.patch_select(torch.from_numpy(case.view_logit).cuda(), case.view_offsets, S,
+                                   case.w_lexical, case.threshold)
+        vk_ref = oracle.patch_select(case.view_logit, case.view_lexical, case.w_lexical, case.threshold)
+        keep_ref = oracle.token_keep_from_views(vk_ref, case.view_offsets, S)
+    g = torch.from_numpy(gamma).cuda()
+    wq_f = lv.tsm_fold_gain(to_device(wq, "bf16"), g)
+    wk_f = lv.tsm_fold_gain(to_device(wk, "bf16"), g)
+    q, k = lv.tsm_qk(to_device(hid, "bf16"), tk, V, wq_f, wk_f, Hq, Hkv, D, eps=eps, rope_theta=theta)
+    torch.cuda.synchronize()
+    if tk is not None:
+        assert np.array_equal(tk.cpu().numpy(), keep_ref)
+    dec = oracle.litevlm.decode_stored
+    qr, kr = OT.tsm_qk(dec(hid, "bf16"), keep_ref, V, gamma.astype(np.float64), dec(wq, "bf16"),
+                       dec(wk, "bf16"), Hq, Hkv, D, eps, theta)
+    return to_float64(q)[:, V:], to_float64(k), qr, kr
+
+
+def check(got, ref, what):
+    err = np.abs(got - ref)
+    bad = err > TSM_ATOL + TSM_RTOL * np.abs(ref)
+    rl2 = row_rel_l2(got, ref)
+    assert not bad.any(), f"{what}: {bad.sum()} elements out of tolerance, max abs {err.max():.3g}"
+    assert rl2.max() <= TSM_ROW_L2, f"{what}: row relative L2 {rl2.max():.3g}"
+    return float(err.max()), float(rl2.max())
+
+
+@pytest.mark.parametrize("name,over,Dm", [
+    ("3 views x 64 + 32 text, one view dropped, D=128", dict(B=2, N=3, Tv=64, T=32, Hq=4, Hkv=2, D=128,
+                                                            n_masked=1), 256),
+    ("ragged rows, D=64, GQA 8/2", dict(B=1, N=2, Tv=100, T=37, Hq=8, Hkv=2, D=64, n_masked=0), 96),
+    ("MHA 16/16 D=128, 2 of 6 views dropped", dict(B=1, N=6, Tv=40, T=64, Hq=16, Hkv=16, D=128,
+                                                   n_masked=2), 512),
+])
+def test_tsm_matches_oracle(name, over, Dm):
+    case = synth.config_case(2, **over)
+    q, k, qr, kr = run(case, Dm, seed=4100)
+    sq = check(q, qr, name + " q")
+    sk = check(k, kr, name + " k")
+    log(f"{name}: q max abs {sq[0]:.2e} row L2 {sq[1]:.2e}; k max abs {sk[0]:.2e} row L2 {sk[1]:.2e}")
+
+
+def test_tsm_without_token_keep_uses_plain_positions():
+    case = synth.config_case(2, B=1, N=2, Tv=64, T=16, Hq=4, Hkv=2, D=128, n_masked=0)
+    q, k, qr, kr = run(case, 128, seed=4200, use_keep=False)
+    check(q, qr, "q")
+    check(k, kr, "k")
+
+
+@pytest.mark.parametrize("cfg", [3, 4])
+def test_tsm_full_size(cfg):
+    """The 6x1024 + 128 shape with model width Hq*D = 4096 (batch 1, and batch 8
+    with 0-4 views dropped per sample): every key row and text query row."""
+    case = synth.config_case(cfg)
+    if cfg == 4:
+        case = synth.config_case(4, B=2)   # two samples keep the float64 oracle within seconds
+    q, k, qr, kr = run(case, case.Hq * case.D, seed=4300 + cfg)
+    sq = check(q, qr, f"cfg{cfg} q")
+    sk = check(k, kr, f"cfg{cfg} k")
+    log(f"cfg{cfg}: q max abs {sq[0]:.2e} row L2 {sq[1]:.2e}; k max abs {sk[0]:.2e} row L2 {sk[1]:.2e}")
