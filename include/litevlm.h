@@ -248,7 +248,7 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
  * bf16. The results are the q and k that litevlm_token_score_topk reads.
  *
  *   B, S, V_full       batch, sequence length, visual tokens (T = S - V_full >= 1)
- *   Dm                 model width: a multiple of 32, at most 65536
+ *   Dm                 model width: a multiple of 64, at most 65536
  *   Hq, Hkv, D         heads (Hq % Hkv == 0), head dim 64 or 128; Hq*D and Hkv*D must
  *                      be multiples of 128 (else LITEVLM_ERR_UNSUPPORTED)
  *   hidden             dev bf16 [B, S, Dm]

@@ -277,7 +277,7 @@ litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm
   if (B < 1 || B > LITEVLM_MAX_BATCH || V_full < 0 || S <= V_full || Hq < 1 || Hkv < 1 ||
       Hq > LITEVLM_MAX_HEADS || Hq % Hkv != 0 || (D != 64 && D != 128))
     return LITEVLM_ERR_BAD_SHAPE;
-  if (Dm < 32 || Dm % 32 != 0 || Dm > 65536) return LITEVLM_ERR_BAD_SHAPE;
+  if (Dm < 64 || Dm % 64 != 0 || Dm > 65536) return LITEVLM_ERR_BAD_SHAPE;
   // a workgroup covers 128 output features: whole heads, rotary partners together
   if ((Hq * D) % 128 != 0 || (Hkv * D) % 128 != 0) return LITEVLM_ERR_UNSUPPORTED;
   if ((int64_t)B * S > INT32_MAX / 2 || (int64_t)B * S * Dm > ((int64_t)1 << 40)) return LITEVLM_ERR_BAD_SHAPE;

@@ -15,25 +15,44 @@
 //   - a wave owns two column blocks that are rotary partners (elements d and
 //     d + D/2 of one head), so the rotation is lane-local in the accumulators.
 //
-// Tiling: a workgroup (4 waves) computes 128 rows x 128 output features; wave
-// (wr, wc) holds rows 64*wr .. +64 and the column blocks c0 and c0 + D/64.
-// A and B tiles of 32 columns of the model width stream global -> LDS directly
-// (global_load_lds_dwordx4) through a 4-stage ring, three stages ahead of the
-// MFMAs, into 64-byte rows whose four 16-byte pieces are XOR-swizzled by
-// (row >> 1) & 3 so that each quarter-wave's operand reads hit distinct banks.
+// Tiling (the defaults below): a workgroup (4 waves) computes 128 rows x 128
+// output features; wave (wr, wc) holds rows 64*wr .. +64 and the column blocks
+// c0 and c0 + D/64. A and B tiles of 64 columns of the model width stream
+// global -> LDS directly (global_load_lds_dwordx4) through a double buffer
+// (66 KB, two workgroups per CU) into 128-byte rows whose 16-byte pieces are
+// XOR-swizzled so that operand reads are free of bank conflicts. Measured
+// alternatives (256-row or 256-feature tiles, 3- to 6-stage rings, 32-column
+// stages) were slower on both the batch-1 and the batch-8 shapes: the workgroups
+// wait on the copies, and what helps is more workgroups per CU, not deeper
+// rings.
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace litevlm {
 namespace {
 
-constexpr int kMT = 128, kNT = 128, kKT = 32, kStages = 4;
+// Tile shape (rows x output features) and ring depth; see the header comment.
+#ifndef TSM_MT
+#define TSM_MT 128
+#endif
+#ifndef TSM_NT
+#define TSM_NT 128
+#endif
+#ifndef TSM_STAGES
+#define TSM_STAGES 2
+#endif
+#ifndef TSM_KT
+#define TSM_KT 64
+#endif
+constexpr int kMT = TSM_MT, kNT = TSM_NT, kKT = TSM_KT, kStages = TSM_STAGES;  // Dm % kKT == 0 (host check)
+constexpr int kPieces = kKT / 8;      // 16-byte pieces per staged row
 constexpr int kRowB = kKT * 2;        // bytes per staged row
 constexpr int kAB = kMT * kRowB;      // A tile bytes per stage
 constexpr int kBB = kNT * kRowB;      // B tile bytes per stage
 constexpr int kStageB = kAB + kBB;
 constexpr int kRingB = kStages * kStageB;
 constexpr int kLdsB = kRingB + kMT * 4 /* row factors */ + kMT * 4 /* positions */ + 64 /* reductions */;
+constexpr int kWgPerCu = (160 * 1024 / kLdsB) >= 4 ? 4 : (160 * 1024 / kLdsB) >= 1 ? 160 * 1024 / kLdsB : 1;
 
 struct TsmParams {
   const uint8_t* x;     // bf16 [B, S, Dm]
@@ -53,7 +72,12 @@ __device__ __forceinline__ void vm_wait() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
-__device__ __forceinline__ int swz(int row) { return (row >> 1) & 3; }
+// XOR swizzle of a staged row's pieces. The LDS serves a 16-byte read for 16
+// lanes per cycle across 64 banks (256 bytes): the 16 consecutive rows such a
+// group reads must put their pieces in distinct 16-byte bank slots. A 256-byte
+// bank window holds 256 / (2*kKT) rows, so rows that share a window position
+// get distinct pieces.
+__device__ __forceinline__ int swz(int row) { return kPieces == 4 ? (row >> 2) & 3 : (row >> 1) & 7; }
 
 // Workgroup barrier that waits only for this wave's LDS operations: the
 // __syncthreads fence would also wait for every direct copy still in flight,
@@ -63,10 +87,19 @@ __device__ __forceinline__ void ring_barrier() { asm volatile("s_waitcnt lgkmcnt
 __device__ __forceinline__ int acc_row(int r, int hl) { return 8 * (r >> 2) + 4 * hl + (r & 3); }
 
 typedef uint32_t u32x4v __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+// x.lo*y.lo + x.hi*y.hi + c on packed bf16 pairs (fp32 accumulate).
+__device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c) {
+  return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, x), __builtin_bit_cast(bf16x2v, y), c, false);
+}
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void tsm_proj_kernel(TsmParams p) {
-  constexpr int PB = D / 64;  // column-block distance of rotary partners
+__global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
+  constexpr int PB = D / 64;       // column-block distance of rotary partners
+  constexpr int RB = kMT / 64;     // 32-row blocks per wave (waves split the rows in two)
+  constexpr int CBW = kNT / 64;    // 32-column blocks per wave (waves split the columns in two)
+  static_assert(CBW == 2 || CBW == 4, "tile width");
   const int L = blockIdx.x;
   const int item = (L & 7) * p.per_xcd + (L >> 3);  // an XCD takes a contiguous item range
   if (item >= p.n_items) return;
@@ -109,47 +142,69 @@ __global__ __launch_bounds__(256, 2) void tsm_proj_kernel(TsmParams p) {
       for (int j = tid; j < row0; j += 256) cnt += kr[j];
 #pragma unroll
     for (int x = 1; x < kWave; x <<= 1) cnt += __shfl_xor(cnt, x, kWave);
-    int f = 0;
-    if (tid < kMT && tid < nrows) f = kr ? kr[row0 + tid] : 1;
-    int incl = f;
-#pragma unroll
-    for (int x = 1; x < kWave; x <<= 1) {
-      const int y = __shfl_up(incl, x, kWave);
-      if (lane >= x) incl += y;
-    }
     if (lane == 0) red[w] = cnt;
-    if (lane == kWave - 1) red[4 + w] = incl;
     __syncthreads();
-    if (tid < kMT) {
-      const int base = kr ? red[0] + red[1] + red[2] + red[3] : row0;
-      pos[tid] = base + (incl - f) + (w == 1 ? red[4] : 0);
+    const int base = kr ? red[0] + red[1] + red[2] + red[3] : row0;
+    for (int t0 = 0; t0 < kMT; t0 += 256) {
+      const int t = t0 + tid;
+      int f = 0;
+      if (t < nrows) f = kr ? kr[row0 + t] : 1;
+      int incl = f;
+#pragma unroll
+      for (int x = 1; x < kWave; x <<= 1) {
+        const int y = __shfl_up(incl, x, kWave);
+        if (lane >= x) incl += y;
+      }
+      __syncthreads();
+      if (lane == kWave - 1) red[4 + w] = incl;
+      __syncthreads();
+      int before = t0 == 0 ? 0 : red[8];  // kept rows of the earlier chunks
+      for (int x = 0; x < w; ++x) before += red[4 + x];
+      if (t < kMT) pos[t] = base + before + (incl - f);
+      __syncthreads();
+      if (tid == 0) red[8] = (t0 == 0 ? 0 : red[8]) + red[4] + red[5] + red[6] + red[7];
     }
   }
 
   // ---- per-lane copy sources (fixed) and operand offsets (fixed)
   // copy j of a wave fills LDS pieces (w + 4j)*64 + lane of the A (resp. B) tile
-  size_t asrc[2], bsrc[2];
+  constexpr int CA = kAB / 4096, CB = kBB / 4096;  // copies per thread per stage
+  size_t asrc[CA], bsrc[CB];
 #pragma unroll
-  for (int j = 0; j < 2; ++j) {
+  for (int j = 0; j < CA; ++j) {
     const int slot = (w + 4 * j) * 64 + lane;
-    const int row = slot >> 2, logical = (slot & 3) ^ swz(slot >> 2);
+    const int row = slot / kPieces, logical = (slot % kPieces) ^ swz(row);
     asrc[j] = ((size_t)((size_t)b * p.S + row0 + min(row, nrows - 1)) * Dm + logical * 8) * 2;
+  }
+#pragma unroll
+  for (int j = 0; j < CB; ++j) {
+    const int slot = (w + 4 * j) * 64 + lane;
+    const int row = slot / kPieces, logical = (slot % kPieces) ^ swz(row);
     bsrc[j] = ((size_t)(n0 + row) * Dm + logical * 8) * 2;
   }
   const uint32_t lds_w = __builtin_amdgcn_readfirstlane((uint32_t)w * 1024u);
-  const int c0 = (D == 128) ? wc : 2 * wc;  // this wave's column blocks: c0 and c0 + PB
-  uint32_t aoff[2][2], boff[2][2];          // [block][k16 step]
+  // this wave's column blocks: rotary partners (blocks PB apart) always together
+  int cbl[CBW];
+  if constexpr (CBW == 4) {
 #pragma unroll
-  for (int ks = 0; ks < 2; ++ks) {
+    for (int i = 0; i < 4; ++i) cbl[i] = 4 * wc + i;
+  } else {
+    cbl[0] = (D == 128) ? wc : 2 * wc;
+    cbl[1] = cbl[0] + PB;
+  }
+  constexpr int KS = kKT / 16;          // k16 steps per stage
+  uint32_t aoff[RB][KS], boff[CBW][KS];  // [block][k16 step]
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
     const int logical = 2 * ks + hl;
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
-      const int row = 64 * wr + 32 * rb + l32;
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = (kMT / 2) * wr + 32 * rb + l32;
       aoff[rb][ks] = row * kRowB + ((logical ^ swz(row)) * 16);
     }
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      const int nrow = 32 * (c0 + c * PB) + l32;
+    for (int c = 0; c < CBW; ++c) {
+      const int nrow = 32 * cbl[c] + l32;
       boff[c][ks] = kAB + nrow * kRowB + ((logical ^ swz(nrow)) * 16);
     }
   }
@@ -158,91 +213,117 @@ __global__ __launch_bounds__(256, 2) void tsm_proj_kernel(TsmParams p) {
     const size_t kb = (size_t)s * kKT * 2;
     uint8_t* st = lds + (s % kStages) * kStageB;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
+    for (int j = 0; j < CA; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(p.x + asrc[j] + kb),
                                        (__attribute__((address_space(3))) void*)(st + lds_w + 4 * j * 1024), 16, 0, 0);
+#pragma unroll
+    for (int j = 0; j < CB; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(W + bsrc[j] + kb),
                                        (__attribute__((address_space(3))) void*)(st + kAB + lds_w + 4 * j * 1024), 16,
                                        0, 0);
-    }
   };
 
-  f32x16 acc[2][2];
+  f32x16 acc[RB][CBW];
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < CBW; ++c)
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[rb][c][r] = 0.f;
-  float ssq[2] = {0.f, 0.f};
+  float ssq[RB];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) ssq[rb] = 0.f;
 
   const int nK = Dm / kKT;
+  constexpr int CS = CA + CB;  // copies per thread per stage
+  static_assert(CS * (kStages - 2) <= 63 && kStages >= 2 && kStages <= 6, "vmcnt range");
   for (int s = 0; s < kStages - 1 && s < nK; ++s) copy_stage(s);
   for (int s = 0; s < nK; ++s) {
-    // stage s has landed once at most the copies of the later issued stages remain
-    if (s + 2 < nK) vm_wait<8>();
-    else if (s + 1 < nK) vm_wait<4>();
+    // stage s has landed once at most the copies of the stages issued after it remain
+    const int later = min(nK - 1, s + kStages - 2) - s;
+    if (later >= 4) vm_wait<4 * CS>();
+    else if (later == 3) vm_wait<3 * CS>();
+    else if (later == 2) vm_wait<2 * CS>();
+    else if (later == 1) vm_wait<CS>();
     else vm_wait<0>();
-    ring_barrier();  // every wave's copies of stage s are visible; ring slot (s-1)%4 is free
+    ring_barrier();  // every wave's copies of stage s are visible; ring slot (s-1)%kStages is free
     if (s + kStages - 1 < nK) copy_stage(s + kStages - 1);
     const uint8_t* st = lds + (s % kStages) * kStageB;
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-      bf16x8 a[2], bo[2];
+    for (int ks = 0; ks < KS; ++ks) {
+      bf16x8 a[RB], bo[CBW];
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb) a[rb] = *reinterpret_cast<const bf16x8*>(st + aoff[rb][ks]);
+      for (int rb = 0; rb < RB; ++rb) a[rb] = *reinterpret_cast<const bf16x8*>(st + aoff[rb][ks]);
 #pragma unroll
-      for (int c = 0; c < 2; ++c) bo[c] = *reinterpret_cast<const bf16x8*>(st + boff[c][ks]);
+      for (int c = 0; c < CBW; ++c) bo[c] = *reinterpret_cast<const bf16x8*>(st + boff[c][ks]);
 #pragma unroll
-      for (int rb = 0; rb < 2; ++rb)
+      for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
-        for (int c = 0; c < 2; ++c) acc[rb][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[rb], bo[c], acc[rb][c], 0, 0, 0);
-      if (wc == 0) {  // row sums of squares, from the A operands (one wave per row half)
+        for (int c = 0; c < CBW; ++c)
+          acc[rb][c] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[rb], bo[c], acc[rb][c], 0, 0, 0);
+      // Row sums of squares from the A operands on the packed bf16 dot unit. The
+      // two waves holding the same rows take alternate k16 steps, so every SIMD
+      // carries the same vector work.
+      if ((ks & 1) == wc) {
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int rb = 0; rb < RB; ++rb) {
           const u32x4v u = __builtin_bit_cast(u32x4v, a[rb]);
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float lo = __uint_as_float(u[e] << 16), hi = __uint_as_float(u[e] & 0xFFFF0000u);
-            ssq[rb] = fmaf(lo, lo, ssq[rb]);
-            ssq[rb] = fmaf(hi, hi, ssq[rb]);
-          }
+          for (int e = 0; e < 4; ++e) ssq[rb] = dot2_bf16(u[e], u[e], ssq[rb]);
         }
       }
     }
   }
 
   // ---- epilogue: RMS factor per row, rotary embedding, bf16 store
-  if (wc == 0) {
+  // (the ring is free now: its first bytes hold the wc = 1 waves' partial sums)
+  float* part = reinterpret_cast<float*>(lds);
+  __syncthreads();
+  if (wc == 1) {
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb) {
+    for (int rb = 0; rb < RB; ++rb) {
       const float tot = sum_xor32(ssq[rb]);
-      if (hl == 0) rs[64 * wr + 32 * rb + l32] = 1.f / sqrtf(tot / (float)Dm + p.eps);
+      if (hl == 0) part[(kMT / 2) * wr + 32 * rb + l32] = tot;
     }
   }
   __syncthreads();
-  const int d = (32 * c0) % D + l32;  // element of the first half of its head (d < D/2)
-  const int head = (n0 + 32 * c0) / D;
-  const double inv_freq = exp2(-(2.0 * d / D) * p.log2_theta);
+  if (wc == 0) {
+#pragma unroll
+    for (int rb = 0; rb < RB; ++rb) {
+      const int row = (kMT / 2) * wr + 32 * rb + l32;
+      const float tot = sum_xor32(ssq[rb]);
+      if (hl == 0) rs[row] = 1.f / sqrtf((tot + part[row]) / (float)Dm + p.eps);
+    }
+  }
+  __syncthreads();
   uint16_t* out = isq ? p.q : p.k;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb)
+  for (int i = 0; i < CBW / 2; ++i) {
+    // slots c (a first-half block) and cp (its partner, PB blocks on) of this wave's list
+    const int c = CBW == 2 ? 0 : (D == 128 ? i : 2 * i);
+    const int cp = CBW == 2 ? 1 : c + PB;
+    const int d = (32 * cbl[c]) % D + l32;  // element of the first half of its head (d < D/2)
+    const int head = (n0 + 32 * cbl[c]) / D;
+    const double inv_freq = exp2(-(2.0 * d / D) * p.log2_theta);
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int row = 64 * wr + 32 * rb + acc_row(r, hl);
-      if (row < nrows) {
-        const float f = rs[row];
-        const float x1 = acc[rb][0][r] * f, x2 = acc[rb][1][r] * f;
-        // angle pos * theta^(-2d/D), reduced to [-pi, pi] in double
-        double a = (double)pos[row] * inv_freq;
-        a -= 6.283185307179586 * rint(a * 0.15915494309189535);
-        float sn, cs;
-        sincosf((float)a, &sn, &cs);
-        uint16_t* o = out + (((size_t)b * p.S + row0 + row) * H + head) * D;
-        o[d] = f32_to_bf16_bits(x1 * cs - x2 * sn);
-        o[d + D / 2] = f32_to_bf16_bits(x2 * cs + x1 * sn);
+    for (int rb = 0; rb < RB; ++rb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int row = (kMT / 2) * wr + 32 * rb + acc_row(r, hl);
+        if (row < nrows) {
+          const float f = rs[row];
+          const float x1 = acc[rb][c][r] * f, x2 = acc[rb][cp][r] * f;
+          // angle pos * theta^(-2d/D), reduced to [-pi, pi] in double
+          double a = (double)pos[row] * inv_freq;
+          a -= 6.283185307179586 * rint(a * 0.15915494309189535);
+          float sn, cs;
+          sincosf((float)a, &sn, &cs);
+          uint16_t* o = out + (((size_t)b * p.S + row0 + row) * H + head) * D;
+          o[d] = f32_to_bf16_bits(x1 * cs - x2 * sn);
+          o[d + D / 2] = f32_to_bf16_bits(x2 * cs + x1 * sn);
+        }
       }
-    }
+  }
 }
 
 // w_out[n, c] = bf16(w[n, c] * gamma[c]): the RMS normalisation gain folded

@@ -238,7 +238,8 @@ def test_tsm_validation():
     assert tq(wk=None) == _abi.ERR_NULL_POINTER
     assert tq(q=None) == _abi.ERR_NULL_POINTER
     assert tq(S=80) == _abi.ERR_BAD_SHAPE                     # no text token
-    assert tq(Dm=100) == _abi.ERR_BAD_SHAPE                   # not a multiple of 32
+    assert tq(Dm=100) == _abi.ERR_BAD_SHAPE                   # not a multiple of 64
+    assert tq(Dm=96) == _abi.ERR_BAD_SHAPE
     assert tq(D=96) == _abi.ERR_BAD_SHAPE
     assert tq(Hkv=3) == _abi.ERR_BAD_SHAPE
     assert tq(Hq=2, Hkv=1, D=64) == _abi.ERR_UNSUPPORTED       # Hkv*D = 64 < 128

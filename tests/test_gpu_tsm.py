@@ -57,7 +57,7 @@ def check(got, ref, what):
 @pytest.mark.parametrize("name,over,Dm", [
     ("3 views x 64 + 32 text, one view dropped, D=128", dict(B=2, N=3, Tv=64, T=32, Hq=4, Hkv=2, D=128,
                                                             n_masked=1), 256),
-    ("ragged rows, D=64, GQA 8/2", dict(B=1, N=2, Tv=100, T=37, Hq=8, Hkv=2, D=64, n_masked=0), 96),
+    ("ragged rows, D=64, GQA 8/2", dict(B=1, N=2, Tv=100, T=37, Hq=8, Hkv=2, D=64, n_masked=0), 192),
     ("MHA 16/16 D=128, 2 of 6 views dropped", dict(B=1, N=6, Tv=40, T=64, Hq=16, Hkv=16, D=128,
                                                    n_masked=2), 512),
 ])
