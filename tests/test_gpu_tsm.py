@@ -42,7 +42,7 @@ def run(case, Dm, seed, eps=EPS, theta=THETA, use_keep=True):
     dec = oracle.litevlm.decode_stored
     qr, kr = OT.tsm_qk(dec(hid, "bf16"), keep_ref, V, gamma.astype(np.float64), dec(wq, "bf16"),
                        dec(wk, "bf16"), Hq, Hkv, D, eps, theta)
-    return to_float64(q)[:, V:], to_float64(k), qr, kr
+    return to_float64(q[:, V:]), to_float64(k), qr, kr
 
 
 def check(got, ref, what):
