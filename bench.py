@@ -358,6 +358,21 @@ def main():
         t1.record(stream)
         torch.cuda.synchronize()
         us = t0.elapsed_time(t1) / iters * 1e3
+        # the kept tokens' hidden states gathered for the LLM (selection from this q, k)
+        r = HEADLINE_R if cfg == 3 else c.keep_ratio
+        sel = lv.token_score_topk(q, k, None, tk, r, c.V_full, gather=False)
+        hc = torch.empty((c.B * c.S, Dm), dtype=torch.bfloat16, device=dev)
+        for _ in range(warmup):
+            lv.gather_hidden(x, sel["kept_index"], sel["cu_seqlens"], out=hc)
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(iters):
+            lv.gather_hidden(x, sel["kept_index"], sel["cu_seqlens"], out=hc)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        g_us = t0.elapsed_time(t1) / iters * 1e3
+        rows = int(sel["cu_seqlens"][-1].item())
+        g_bytes = 2.0 * rows * Dm * 2
         T = c.S - c.V_full
         kept = int(nv.sum().item()) + c.B * T
         fl_alg = 2.0 * Dm * (kept * c.Hkv * c.D + c.B * T * c.Hq * c.D)
@@ -367,7 +382,10 @@ def main():
                 "tflops": round(fl_alg / (us * 1e-6) / 1e12, 1),
                 "frac_bf16_peak": round(fl_alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
                 "note": "keys of the kept tokens and queries of the text tokens count as algorithmic; "
-                        "the kernel also projects the keys of dropped views' tokens"}
+                        "the kernel also projects the keys of dropped views' tokens",
+                "gather_hidden": {"keep_ratio": r, "rows": rows, "us": round(g_us, 2),
+                                  "gbs": round(g_bytes / (g_us * 1e-6) / 1e9, 1),
+                                  "frac_hbm": round(g_bytes / (g_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
 
     if args.workload == 3:
         main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])

@@ -11,7 +11,8 @@
  *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
  * in front of the scoring, from the hidden states:
  *   litevlm_tsm_qk            the Token Selection Module's scoring queries and keys
- *                             (litevlm_tsm_fold_gain prepares its weights)
+ *                             (litevlm_tsm_fold_gain prepares its weights;
+ *                             litevlm_gather_hidden compacts the hidden states for the LLM)
  * and, for the token generated after the prefill:
  *   litevlm_decode_attn       extend-one decode attention over the compacted KV cache
  *
@@ -265,6 +266,27 @@ litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm
                                 int32_t D, const void* hidden, const uint8_t* token_keep, const void* w_q,
                                 const void* w_k, float eps, float rope_theta, void* q, void* k,
                                 void* stream);
+
+/*
+ * litevlm_gather_hidden - the compacted hidden states for the LLM: packed row r
+ * of sample b (rows cu_seqlens[b]..cu_seqlens[b+1]-1) is an exact copy of row
+ * kept_index[r] of that sample's hidden states.
+ *
+ * Paper: Design section, Token Selection Module paragraph (the pruned visual
+ * tokens do not enter the LLM: what the LLM prefills is the kept tokens' hidden
+ * states, which its own first layer projects).
+ *
+ *   B, S               batch, rows per sample of hidden
+ *   row_bytes          bytes per row (a multiple of 16, at most 196608)
+ *   hidden             dev [B, S, row_bytes]
+ *   kept_index, cu_seqlens   dev int32, as written by litevlm_token_score_topk
+ *                      (values of kept_index must lie in [0, S))
+ *   out                dev [total, row_bytes], total = cu_seqlens[B] (capacity B*S rows;
+ *                      rows past total are untouched)
+ */
+litevlm_status_t litevlm_gather_hidden(int32_t B, int32_t S, int32_t row_bytes, const void* hidden,
+                                       const int32_t* kept_index, const int32_t* cu_seqlens, void* out,
+                                       void* stream);
 
 /*
  * litevlm_tsm_fold_gain - w_out[n, c] = bf16(w[n, c] * gamma[c]): folds the RMS

@@ -23,6 +23,7 @@ from . import _abi
 from ._abi import LiteVLMError, load  # noqa: F401
 
 __all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "tsm_qk", "tsm_fold_gain",
+           "gather_hidden",
            "dtype_code",
            "workspace_bytes", "decode_workspace_bytes", "LiteVLMError", "load"]
 
@@ -206,3 +207,17 @@ def tsm_qk(hidden: torch.Tensor, token_keep: Optional[torch.Tensor], V_full: int
                                _ptr(w_k), float(eps), float(rope_theta), _ptr(q), _ptr(k), _stream(dev))
     _abi.check(st, "litevlm_tsm_qk")
     return q, k
+
+
+def gather_hidden(hidden: torch.Tensor, kept_index: torch.Tensor, cu_seqlens: torch.Tensor,
+                  out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Packed copies of the kept rows of hidden [B,S,...] (rows cu_seqlens[b].. of the
+    result for sample b): out [B*S, ...] with rows past cu_seqlens[B] untouched."""
+    B, S = hidden.shape[0], hidden.shape[1]
+    row_bytes = hidden[0, 0].numel() * hidden.element_size()
+    o = out if out is not None else torch.empty((B * S,) + tuple(hidden.shape[2:]), dtype=hidden.dtype,
+                                                device=hidden.device)
+    st = load().litevlm_gather_hidden(B, S, row_bytes, _ptr(hidden), _ptr(kept_index), _ptr(cu_seqlens),
+                                      _ptr(o), _stream(hidden.device))
+    _abi.check(st, "litevlm_gather_hidden")
+    return o

@@ -261,6 +261,18 @@ litevlm_status_t litevlm_decode_attn(int32_t in_dtype, int32_t out_dtype, int32_
   return hip_status(launch_decode_attn(a, static_cast<hipStream_t>(stream)));
 }
 
+litevlm_status_t litevlm_gather_hidden(int32_t B, int32_t S, int32_t row_bytes, const void* hidden,
+                                       const int32_t* kept_index, const int32_t* cu_seqlens, void* out,
+                                       void* stream) {
+  if (!hidden || !kept_index || !cu_seqlens || !out) return LITEVLM_ERR_NULL_POINTER;
+  if (B < 1 || B > LITEVLM_MAX_BATCH || S < 1 || (int64_t)B * S > INT32_MAX / 2) return LITEVLM_ERR_BAD_SHAPE;
+  if (row_bytes < 16 || row_bytes % 16 != 0 || row_bytes > 48 * 256 * 16) return LITEVLM_ERR_BAD_SHAPE;
+  if (!aligned(hidden, 16) || !aligned(out, 16) || !aligned(kept_index, 4) || !aligned(cu_seqlens, 4))
+    return LITEVLM_ERR_MISALIGNED;
+  return hip_status(launch_gather_hidden(B, S, row_bytes, hidden, kept_index, cu_seqlens, out,
+                                         static_cast<hipStream_t>(stream)));
+}
+
 litevlm_status_t litevlm_tsm_fold_gain(int32_t rows, int32_t cols, const void* w, const float* gamma,
                                        void* w_out, void* stream) {
   if (!w || !gamma || !w_out) return LITEVLM_ERR_NULL_POINTER;

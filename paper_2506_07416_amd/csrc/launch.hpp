@@ -47,6 +47,15 @@ struct ScoreArgs {
 };
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream);
 
+// Row gather behind the compaction: rows kept_index[r] of each sample of q, k,
+// v (qvec / kvvec 16-byte pieces per row) into packed qc, kc, vc (each may be
+// NULL, kvvec may be 0).
+void launch_gather(int B, int S, const int32_t* kept_index, const int32_t* cu_seqlens, const void* q,
+                   const void* k, const void* v, void* qc, void* kc, void* vc, int qvec, int kvvec,
+                   hipStream_t stream);
+hipError_t launch_gather_hidden(int B, int S, int row_bytes, const void* hidden, const int32_t* kept_index,
+                                const int32_t* cu_seqlens, void* out, hipStream_t stream);
+
 struct AttnArgs {
   int in_dtype, out_dtype, B, Hq, Hkv, D, max_seqlen, causal;
   const void* q;

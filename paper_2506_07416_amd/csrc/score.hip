@@ -1435,29 +1435,41 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
                      a.keep_ratio, a.token_keep, acc, inv, a.scores, a.kept_index, a.cu_seqlens);
   if (a.qc || a.kc || a.vc) {
     const int esz = a.dtype == LITEVLM_F32 ? 4 : (a.dtype == LITEVLM_BF16 ? 2 : 1);
-    const int qvec = a.Hq * a.D * esz / 16, kvvec = a.Hkv * a.D * esz / 16;
-    const int rows = a.B * a.S;
-    auto launch = [&](auto kernel, int rpi) {
-      const int grid = std::max(1, std::min(1024, (rows + rpi - 1) / rpi));
-      hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, stream, a.B, a.S, a.kept_index,
-                         a.cu_seqlens, static_cast<const u32x4*>(a.q), static_cast<const u32x4*>(a.k),
-                         static_cast<const u32x4*>(a.v), static_cast<u32x4*>(a.qc),
-                         static_cast<u32x4*>(a.kc), static_cast<u32x4*>(a.vc), qvec, kvvec);
-    };
-    // 16-byte pieces per thread and row, (Q + K + V pieces) / 256: at most
-    // (4096 + 2*4096) / 256 = 48 with Hq <= LITEVLM_MAX_HEADS; about 24 loads
-    // in flight per thread
-    const int ppt = (qvec + 2 * kvvec + 255) / 256;
-    if (ppt <= 1) launch(gather_rows_kernel<1, 8>, 8);
-    else if (ppt <= 2) launch(gather_rows_kernel<2, 8>, 8);
-    else if (ppt <= 3) launch(gather_rows_kernel<3, 8>, 8);
-    else if (ppt <= 4) launch(gather_rows_kernel<4, 6>, 6);
-    else if (ppt <= 6) launch(gather_rows_kernel<6, 4>, 4);
-    else if (ppt <= 12) launch(gather_rows_kernel<12, 2>, 2);
-    else if (ppt <= 24) launch(gather_rows_kernel<24, 1>, 1);
-    else launch(gather_rows_kernel<48, 1>, 1);
+    launch_gather(a.B, a.S, a.kept_index, a.cu_seqlens, a.q, a.k, a.v, a.qc, a.kc, a.vc,
+                  a.Hq * a.D * esz / 16, a.Hkv * a.D * esz / 16, stream);
   }
 
+  return hipGetLastError();
+}
+
+void launch_gather(int B, int S, const int32_t* kept_index, const int32_t* cu_seqlens, const void* q,
+                   const void* k, const void* v, void* qc, void* kc, void* vc, int qvec, int kvvec,
+                   hipStream_t stream) {
+  const int rows = B * S;
+  auto launch = [&](auto kernel, int rpi) {
+    const int grid = std::max(1, std::min(1024, (rows + rpi - 1) / rpi));
+    hipLaunchKernelGGL(kernel, dim3(grid), dim3(256), 0, stream, B, S, kept_index, cu_seqlens,
+                       static_cast<const u32x4*>(q), static_cast<const u32x4*>(k), static_cast<const u32x4*>(v),
+                       static_cast<u32x4*>(qc), static_cast<u32x4*>(kc), static_cast<u32x4*>(vc), qvec, kvvec);
+  };
+  // 16-byte pieces per thread and row, (Q + K + V pieces) / 256: at most
+  // (4096 + 2*4096) / 256 = 48 with Hq <= LITEVLM_MAX_HEADS (or a hidden-state
+  // row of up to 196 KB); about 24 loads in flight per thread
+  const int ppt = (qvec + 2 * kvvec + 255) / 256;
+  if (ppt <= 1) launch(gather_rows_kernel<1, 8>, 8);
+  else if (ppt <= 2) launch(gather_rows_kernel<2, 8>, 8);
+  else if (ppt <= 3) launch(gather_rows_kernel<3, 8>, 8);
+  else if (ppt <= 4) launch(gather_rows_kernel<4, 6>, 6);
+  else if (ppt <= 6) launch(gather_rows_kernel<6, 4>, 4);
+  else if (ppt <= 12) launch(gather_rows_kernel<12, 2>, 2);
+  else if (ppt <= 24) launch(gather_rows_kernel<24, 1>, 1);
+  else launch(gather_rows_kernel<48, 1>, 1);
+}
+
+hipError_t launch_gather_hidden(int B, int S, int row_bytes, const void* hidden, const int32_t* kept_index,
+                                const int32_t* cu_seqlens, void* out, hipStream_t stream) {
+  launch_gather(B, S, kept_index, cu_seqlens, hidden, nullptr, nullptr, out, nullptr, nullptr, row_bytes / 16, 0,
+                stream);
   return hipGetLastError();
 }
 

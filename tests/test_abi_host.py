@@ -251,3 +251,18 @@ def test_tsm_validation():
     assert lib.litevlm_tsm_fold_gain(4, 8, None, A, A, None) == _abi.ERR_NULL_POINTER
     assert lib.litevlm_tsm_fold_gain(0, 8, A, A, A, None) == _abi.ERR_BAD_SHAPE
     assert lib.litevlm_tsm_fold_gain(4, 8, A, A + 2, A, None) == _abi.ERR_MISALIGNED
+
+
+def test_gather_hidden_validation():
+    lib = lv.load()
+
+    def gh(B=2, S=100, rb=8192, h=A, ki=A, cu=A, o=A):
+        return lib.litevlm_gather_hidden(B, S, rb, h, ki, cu, o, None)
+    assert gh(h=None) == _abi.ERR_NULL_POINTER
+    assert gh(cu=None) == _abi.ERR_NULL_POINTER
+    assert gh(B=0) == _abi.ERR_BAD_SHAPE
+    assert gh(rb=8) == _abi.ERR_BAD_SHAPE
+    assert gh(rb=8200) == _abi.ERR_BAD_SHAPE
+    assert gh(rb=48 * 256 * 16 + 16) == _abi.ERR_BAD_SHAPE
+    assert gh(h=MIS) == _abi.ERR_MISALIGNED
+    assert gh(ki=A + 2) == _abi.ERR_MISALIGNED

@@ -87,3 +87,50 @@ def test_tsm_full_size(cfg):
     sq = check(q, qr, f"cfg{cfg} q")
     sk = check(k, kr, f"cfg{cfg} k")
     log(f"cfg{cfg}: q max abs {sq[0]:.2e} row L2 {sq[1]:.2e}; k max abs {sk[0]:.2e} row L2 {sk[1]:.2e}")
+
+
+@pytest.mark.parametrize("cfg,B", [(2, 1), (4, 3)])
+def test_tsm_scoring_chain_and_hidden_gather(cfg, B):
+    """The selection path from hidden states: patch select, TSM q/k, scoring with
+    no Q/K/V copies, then the hidden states of the kept tokens gathered for the
+    LLM. The gathered rows are exact copies at the GPU's kept indices; the
+    lengths follow the k rule; the scores agree with the oracle's scores from the
+    oracle's own q/k to within the effect of the bf16 q/k rounding."""
+    case = synth.config_case(cfg, B=B) if cfg == 4 else synth.config_case(cfg)
+    Dm = case.Hq * case.D
+    hid, gamma, wq, wk = synth.tsm_inputs(case.B, case.S, Dm, case.Hq, case.Hkv, case.D, seed=4400 + cfg)
+    _, tk, nv = lv.patch_select(torch.from_numpy(case.view_logit).cuda(), case.view_offsets, case.S,
+                                case.w_lexical, case.threshold)
+    g = torch.from_numpy(gamma).cuda()
+    x = to_device(hid, "bf16")
+    q, k = lv.tsm_qk(x, tk, case.V_full, lv.tsm_fold_gain(to_device(wq, "bf16"), g),
+                     lv.tsm_fold_gain(to_device(wk, "bf16"), g), case.Hq, case.Hkv, case.D, eps=EPS,
+                     rope_theta=THETA)
+    out = lv.token_score_topk(q, k, None, tk, case.keep_ratio, case.V_full, gather=False)
+    hc = lv.gather_hidden(x, out["kept_index"], out["cu_seqlens"])
+    torch.cuda.synchronize()
+    cu = out["cu_seqlens"].cpu().numpy()
+    ki = out["kept_index"][:cu[-1]].cpu().numpy()
+    got = hc[:cu[-1]].cpu().view(torch.int16).numpy().view(np.uint16)
+    want = np.concatenate([hid[b, ki[cu[b]:cu[b + 1]]] for b in range(case.B)])
+    assert np.array_equal(got, want), "gathered hidden rows differ from the input rows"
+    # lengths: k rule on the oracle's own patch selection
+    vk = oracle.patch_select(case.view_logit, case.view_lexical, case.w_lexical, case.threshold)
+    tk_ref = oracle.token_keep_from_views(vk, case.view_offsets, case.S)
+    V_b = tk_ref[:, :case.V_full].sum(axis=1)
+    k_b = [oracle.keep_count(case.keep_ratio, int(v)) for v in V_b]
+    assert np.array_equal(np.diff(cu), np.array(k_b) + (case.S - case.V_full))
+    # scores against the oracle's scores from its float64 q/k
+    dec = oracle.litevlm.decode_stored
+    qr, kr = OT.tsm_qk(dec(hid, "bf16"), tk_ref, case.V_full, gamma.astype(np.float64), dec(wq, "bf16"),
+                       dec(wk, "bf16"), case.Hq, case.Hkv, case.D, EPS, THETA)
+    qfull = np.zeros((case.B, case.S, case.Hq, case.D))
+    qfull[:, case.V_full:] = qr
+    ref = oracle.token_scores(qfull, kr, tk_ref, case.V_full, case.Hq, case.Hkv, 1.0 / np.sqrt(case.D))
+    s = out["scores"].cpu().numpy().astype(np.float64)
+    fin = np.isfinite(ref)
+    assert np.array_equal(fin, np.isfinite(s))
+    rel = np.abs(s[fin] - ref[fin]) / ref[fin]
+    log(f"cfg{cfg} B={case.B}: score rel err from bf16 q/k median {np.median(rel):.2e} max {rel.max():.2e}; "
+        f"lengths {np.diff(cu).tolist()}")
+    assert np.median(rel) < 1e-2 and rel.max() < 1e-1
