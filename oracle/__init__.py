@@ -25,3 +25,4 @@ from .litevlm import (  # noqa: F401
     run_path,
 )
 from . import tsm  # noqa: F401,E402  (the Token Selection Module front end)
+from . import psm  # noqa: F401,E402  (the Patch Selection Module forward pass)

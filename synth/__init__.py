@@ -248,3 +248,35 @@ def tsm_inputs(B: int, S: int, Dm: int, Hq: int, Hkv: int, D: int, seed: int):
     w_q = rng.standard_normal((Hq * D, Dm), dtype=np.float32) / np.float32(np.sqrt(Dm))
     w_k = rng.standard_normal((Hkv * D, Dm), dtype=np.float32) / np.float32(np.sqrt(Dm))
     return _to_bf16_bits(hidden), gamma, _to_bf16_bits(w_q), _to_bf16_bits(w_k)
+
+
+def psm_inputs(B: int, T: int, d: int, d_ff: int, n_views: int, n_layers: int, seed: int):
+    """Inputs of the Patch Selection Module forward pass: text token embeddings
+    [B, T, d] from N(0,1) and the flat float32 parameter vector in the order the
+    C ABI documents (per layer: LN1 gain, bias; QKV weight [3d, d], bias; output
+    weight [d, d], bias; LN2 gain, bias; up weight [d_ff, d], bias; down weight
+    [d, d_ff], bias; then final LN gain, bias; latents [N, d]; cross Q, K, V
+    weights [d, d] with biases; head weights [N, d], biases [N]). Gains are
+    1 + 0.1*N(0,1), biases 0.02*N(0,1), weights N(0, 1/fan_in), latents N(0,1).
+    Returns (emb float32 [B, T, d], params float32)."""
+    rng = np.random.Generator(np.random.PCG64(seed))
+    emb = rng.standard_normal((B, T, d), dtype=np.float32)
+    segs = []
+
+    def gain(n):
+        segs.append(1.0 + 0.1 * rng.standard_normal(n))
+
+    def bias(n):
+        segs.append(0.02 * rng.standard_normal(n))
+
+    def weight(rows, fan_in):
+        segs.append(rng.standard_normal(rows * fan_in) / np.sqrt(fan_in))
+
+    for _ in range(n_layers):
+        gain(d), bias(d), weight(3 * d, d), bias(3 * d), weight(d, d), bias(d)
+        gain(d), bias(d), weight(d_ff, d), bias(d_ff), weight(d, d_ff), bias(d)
+    gain(d), bias(d)
+    segs.append(rng.standard_normal(n_views * d))
+    weight(d, d), bias(d), weight(d, d), bias(d), weight(d, d), bias(d)
+    weight(n_views, d), bias(n_views)
+    return emb, np.concatenate(segs).astype(np.float32)
