@@ -387,6 +387,51 @@ def main():
                                   "gbs": round(g_bytes / (g_us * 1e-6) / 1e9, 1),
                                   "frac_hbm": round(g_bytes / (g_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}
 
+    def measure_psm(B, label, T=128, d=256, H=4, dff=1024, N=6, L=4, reps=20):
+        """The Patch Selection Module forward pass (litevlm_psm_forward) on seeded
+        embeddings and parameters; the call's launches captured in a HIP graph and
+        replayed (GPU time), and the eager call timed with events (host-bound)."""
+        emb, par = synth.psm_inputs(B, T, d, dff, N, L, seed=41)
+        e = torch.from_numpy(emb).to(dev)
+        p = torch.from_numpy(par).to(dev)
+        o = torch.empty((B, N), dtype=torch.float32, device=dev)
+        ws = torch.empty((int(lv.load().litevlm_psm_workspace(B, T, d, H, dff)),), dtype=torch.uint8, device=dev)
+        for _ in range(3):
+            lv.psm_forward(e, p, H, dff, N, L, out=o, workspace=ws)
+        torch.cuda.synchronize()
+        t0 = torch.cuda.Event(enable_timing=True)
+        t1 = torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            lv.psm_forward(e, p, H, dff, N, L, out=o, workspace=ws)
+        t1.record(stream)
+        torch.cuda.synchronize()
+        eager_us = t0.elapsed_time(t1) / reps * 1e3
+        side = torch.cuda.Stream()
+        side.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(side):
+            lv.psm_forward(e, p, H, dff, N, L, out=o, workspace=ws)
+        torch.cuda.current_stream().wait_stream(side)
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            lv.psm_forward(e, p, H, dff, N, L, out=o, workspace=ws)
+        g.replay()
+        torch.cuda.synchronize()
+        t0.record(stream)
+        for _ in range(reps):
+            g.replay()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        graph_us = t0.elapsed_time(t1) / reps * 1e3
+        del g
+        M = B * T
+        fl = L * (2.0 * M * (3 * d * d + d * d + 2 * d * dff) + 4.0 * B * T * T * d) + 2.0 * M * 2 * d * d \
+            + B * N * (2.0 * d * d + 4.0 * T * d)
+        return {"workload": label, "layers": L, "tokens": T, "width": d, "heads": H, "d_ff": dff, "views": N,
+                "graph_us": round(graph_us, 2), "eager_us": round(eager_us, 2), "gflop": round(fl / 1e9, 3),
+                "tflops_graph": round(fl / (graph_us * 1e-6) / 1e12, 2),
+                "note": "32 dependent launches of a small network: latency-bound, reported for completeness"}
+
     if args.workload == 3:
         main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])
     else:
@@ -430,8 +475,10 @@ def main():
                           "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                           "attn_frac_bf16_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
 
-    secondary, decode_lines, tsm_lines = [], [], []
+    secondary, decode_lines, tsm_lines, psm_lines = [], [], [], []
     if not args.no_sweep:
+        psm_lines.append(measure_psm(1, "text query of 128 tokens, batch 1"))
+        psm_lines.append(measure_psm(8, "text query of 128 tokens, batch 8"))
         tsm_lines.append(measure_tsm(3, "6 views x 1024 + 128 text, batch 1, GQA 32/8, D=128, model width 4096"))
         tsm_lines.append(measure_tsm(4, "batch 8 ragged (0-4 of 6 views dropped per sample), same shape"))
         torch.cuda.empty_cache()
@@ -500,6 +547,7 @@ def main():
         "secondary": secondary,
         "decode": decode_lines,
         "tsm_front_end": tsm_lines,
+        "psm_forward": psm_lines,
     }
     if not args.no_sweep:
         def run_steps(n):

@@ -4,7 +4,8 @@
  * Paper: "LiteVLM: A Low-Latency Vision-Language Model Inference Pipeline for
  * Resource-Constrained Environments" (arXiv 2506.07416).
  *
- * Three calls, in pipeline order, all enqueued on one HIP stream:
+ * Calls in pipeline order, all enqueued on one HIP stream:
+ *   litevlm_psm_forward       the Patch Selection Module's view logits from the query
  *   litevlm_patch_select      view selection and per-view patch masking
  *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
  *                             (litevlm_token_score_topk_rows: the last n text rows only)
@@ -266,6 +267,54 @@ litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm
                                 int32_t D, const void* hidden, const uint8_t* token_keep, const void* w_q,
                                 const void* w_k, float eps, float rope_theta, void* q, void* k,
                                 void* stream);
+
+/* Number of float32 parameters of the Patch Selection Module (0 if a size is < 1). */
+size_t litevlm_psm_param_count(int32_t d, int32_t d_ff, int32_t n_views, int32_t n_layers);
+
+/* Bytes of device workspace litevlm_psm_forward needs (0 when the sizes are invalid). */
+size_t litevlm_psm_workspace(int32_t B, int32_t T, int32_t d, int32_t n_heads, int32_t d_ff);
+
+/*
+ * litevlm_psm_forward - the Patch Selection Module: view logits from the text
+ * query's token embeddings.
+ *
+ * Paper: Design section, Patch Selection Module paragraph (a small transformer
+ * encoder of 4 layers over the tokenised query; a cross-attention with N
+ * learnable latent queries, one per camera view; each view's result mapped to
+ * an independent logit). Its logits are the view_logit of litevlm_patch_select.
+ *
+ * Per sample, with h = emb (T tokens of width d):
+ *   each of n_layers layers:  h += MHA(LN1(h));  h += W_down GELU(W_up LN2(h) + b_up) + b_down
+ *     (pre-norm; LayerNorm eps 1e-5 with gain and bias; MHA with n_heads heads and
+ *     biased in/out projections; exact erf GELU)
+ *   X = LNf(h);  q_v = latent_v W_cq^T + b_cq;  K = X W_ck^T + b_ck;  V = X W_cv^T + b_cv
+ *   logit_v = w_head_v . (softmax(q_v K^T / sqrt(d)) V) + b_head_v
+ * The GEMM and attention inputs are rounded to bf16 (MFMA, fp32 accumulation);
+ * the residual stream, the norms and the cross-attention run in fp32.
+ *
+ *   B, T               batch (1..LITEVLM_MAX_BATCH), query tokens (1..8192)
+ *   d, n_heads, d_ff   width 256 or 512; d / n_heads = 64 or 128 (else
+ *                      LITEVLM_ERR_UNSUPPORTED); d_ff a multiple of 64 (<= 16384)
+ *   n_views, n_layers  N (1..LITEVLM_MAX_VIEWS), encoder layers (1..64)
+ *   emb                dev fp32 [B, T, d]
+ *   params             dev fp32, n_params = litevlm_psm_param_count(d, d_ff, n_views,
+ *                      n_layers) values in this order: per layer ln1 gain [d], ln1 bias
+ *                      [d], QKV weight [3d, d] (rows: q, k, v outputs), QKV bias [3d],
+ *                      output weight [d, d], output bias [d], ln2 gain [d], ln2 bias [d],
+ *                      up weight [d_ff, d], up bias [d_ff], down weight [d, d_ff], down
+ *                      bias [d]; then final-norm gain [d], bias [d], latents [N, d],
+ *                      cross Q weight [d, d], bias [d], cross K weight [d, d], bias [d],
+ *                      cross V weight [d, d], bias [d], head weights [N, d], head biases [N]
+ *                      (a weight [out, in] maps x to x W^T); another count gives
+ *                      LITEVLM_ERR_BAD_SHAPE
+ *   view_logit         dev out fp32 [B, n_views]
+ *   workspace          dev scratch of litevlm_psm_workspace() bytes (contents on entry
+ *                      ignored; calls that may run concurrently must not share one)
+ */
+litevlm_status_t litevlm_psm_forward(int32_t B, int32_t T, int32_t d, int32_t n_heads, int32_t d_ff,
+                                     int32_t n_views, int32_t n_layers, const float* emb, const float* params,
+                                     size_t n_params, float* view_logit, void* workspace,
+                                     size_t workspace_bytes, void* stream);
 
 /*
  * litevlm_gather_hidden - the compacted hidden states for the LLM: packed row r

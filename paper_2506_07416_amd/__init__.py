@@ -5,6 +5,7 @@ placement and shapes, allocates outputs with PyTorch (device memory and the
 current stream are all PyTorch provides) and passes raw pointers. Every step of
 the path runs in the library's HIP kernels:
 
+    psm_forward(...)       the Patch Selection Module's view logits from the query embeddings
     patch_select(...)      view selection and per-view patch masking
     token_score_topk(...)  visual-token scoring, top-k and gather compaction
     prefill_attn(...)      causal GQA prefill attention over the packed sequence
@@ -23,7 +24,7 @@ from . import _abi
 from ._abi import LiteVLMError, load  # noqa: F401
 
 __all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "tsm_qk", "tsm_fold_gain",
-           "gather_hidden",
+           "gather_hidden", "psm_forward",
            "dtype_code",
            "workspace_bytes", "decode_workspace_bytes", "LiteVLMError", "load"]
 
@@ -220,4 +221,23 @@ def gather_hidden(hidden: torch.Tensor, kept_index: torch.Tensor, cu_seqlens: to
     st = load().litevlm_gather_hidden(B, S, row_bytes, _ptr(hidden), _ptr(kept_index), _ptr(cu_seqlens),
                                       _ptr(o), _stream(hidden.device))
     _abi.check(st, "litevlm_gather_hidden")
+    return o
+
+
+def psm_forward(emb: torch.Tensor, params: torch.Tensor, n_heads: int, d_ff: int, n_views: int,
+                n_layers: int, out: Optional[torch.Tensor] = None,
+                workspace: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """View logits [B, n_views] fp32 from fp32 token embeddings [B, T, d] and the
+    flat fp32 parameter vector (order documented in include/litevlm.h)."""
+    lib = load()
+    B, T, d = emb.shape
+    dev = emb.device
+    o = out if out is not None else torch.empty((B, n_views), dtype=torch.float32, device=dev)
+    if workspace is None:
+        nbytes = int(lib.litevlm_psm_workspace(B, T, d, n_heads, d_ff))
+        workspace = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    st = lib.litevlm_psm_forward(B, T, d, n_heads, d_ff, n_views, n_layers, _ptr(emb), _ptr(params),
+                                 params.numel(), _ptr(o), _ptr(workspace),
+                                 workspace.numel() * workspace.element_size(), _stream(dev))
+    _abi.check(st, "litevlm_psm_forward")
     return o

@@ -36,6 +36,9 @@ SIGNATURES = {
                               _vp, _vp, _vp]),
     "litevlm_tsm_fold_gain": (_i32, [_i32, _i32, _vp, _vp, _vp, _vp]),
     "litevlm_gather_hidden": (_i32, [_i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp]),
+    "litevlm_psm_param_count": (_sz, [_i32, _i32, _i32, _i32]),
+    "litevlm_psm_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32]),
+    "litevlm_psm_forward": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _sz, _vp, _vp, _sz, _vp]),
     "litevlm_decode_attn_workspace": (_sz, [_i32, _i32, _i32, _i32, _i32, _i32]),
     "litevlm_decode_attn": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _vp, _vp,
                                    _i32, _f32, _f32, _f32, _f32, _vp, _vp, _sz, _vp]),

@@ -16,7 +16,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 OBJDIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "liblitevlm.so")
-SOURCES = ["api.hip", "patch_select.hip", "score.hip", "attn.hip", "decode.hip", "tsm.hip"]
+SOURCES = ["api.hip", "patch_select.hip", "score.hip", "attn.hip", "decode.hip", "tsm.hip", "psm.hip"]
 
 HIPCC = os.environ.get("HIPCC", shutil.which("hipcc") or "/opt/rocm/bin/hipcc")
 FLAGS = [

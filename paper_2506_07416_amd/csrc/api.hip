@@ -273,6 +273,58 @@ litevlm_status_t litevlm_gather_hidden(int32_t B, int32_t S, int32_t row_bytes, 
                                          static_cast<hipStream_t>(stream)));
 }
 
+// Patch Selection Module sizes: d 256 or 512 (the LayerNorm and cross kernels
+// hold a row in registers / LDS), head dim d / n_heads of 64 or 128 (the
+// prefill attention kernel), d_ff a multiple of 64.
+static litevlm_status_t check_psm_shape(int32_t B, int32_t T, int32_t d, int32_t n_heads, int32_t d_ff,
+                                 int32_t n_views, int32_t n_layers) {
+  if (B < 1 || B > LITEVLM_MAX_BATCH || T < 1 || T > 8192 || n_views < 1 || n_views > LITEVLM_MAX_VIEWS ||
+      n_layers < 1 || n_layers > 64)
+    return LITEVLM_ERR_BAD_SHAPE;
+  if ((d != 256 && d != 512) || n_heads < 1 || d % n_heads != 0) return LITEVLM_ERR_BAD_SHAPE;
+  const int dh = d / n_heads;
+  if (dh != 64 && dh != 128) return LITEVLM_ERR_UNSUPPORTED;
+  if (d_ff < 64 || d_ff % 64 != 0 || d_ff > 16384) return LITEVLM_ERR_BAD_SHAPE;
+  return LITEVLM_OK;
+}
+
+size_t litevlm_psm_param_count(int32_t d, int32_t d_ff, int32_t n_views, int32_t n_layers) {
+  if (d < 1 || d_ff < 1 || n_views < 1 || n_layers < 1) return 0;
+  return psm_layout(1, 1, d, d_ff, n_views, n_layers).params;
+}
+
+size_t litevlm_psm_workspace(int32_t B, int32_t T, int32_t d, int32_t n_heads, int32_t d_ff) {
+  if (check_psm_shape(B, T, d, n_heads, d_ff, 1, 1) != LITEVLM_OK) return 0;
+  return psm_layout(B, T, d, d_ff, 1, 1).total;
+}
+
+litevlm_status_t litevlm_psm_forward(int32_t B, int32_t T, int32_t d, int32_t n_heads, int32_t d_ff,
+                                     int32_t n_views, int32_t n_layers, const float* emb, const float* params,
+                                     size_t n_params, float* view_logit, void* workspace,
+                                     size_t workspace_bytes, void* stream) {
+  if (!emb || !params || !view_logit) return LITEVLM_ERR_NULL_POINTER;
+  const litevlm_status_t sh = check_psm_shape(B, T, d, n_heads, d_ff, n_views, n_layers);
+  if (sh != LITEVLM_OK) return sh;
+  const PsmLayout L = psm_layout(B, T, d, d_ff, n_views, n_layers);
+  if (n_params != L.params) return LITEVLM_ERR_BAD_SHAPE;
+  if (!aligned(emb, 16) || !aligned(params, 16) || !aligned(view_logit, 4) || (workspace && !aligned(workspace, 16)))
+    return LITEVLM_ERR_MISALIGNED;
+  if (!workspace || workspace_bytes < L.total) return LITEVLM_ERR_WORKSPACE;
+  PsmArgs a;
+  a.B = B;
+  a.T = T;
+  a.d = d;
+  a.n_heads = n_heads;
+  a.d_ff = d_ff;
+  a.n_views = n_views;
+  a.n_layers = n_layers;
+  a.emb = emb;
+  a.params = params;
+  a.view_logit = view_logit;
+  a.workspace = workspace;
+  return hip_status(launch_psm_forward(a, static_cast<hipStream_t>(stream)));
+}
+
 litevlm_status_t litevlm_tsm_fold_gain(int32_t rows, int32_t cols, const void* w, const float* gamma,
                                        void* w_out, void* stream) {
   if (!w || !gamma || !w_out) return LITEVLM_ERR_NULL_POINTER;

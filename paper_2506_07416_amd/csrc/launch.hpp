@@ -103,6 +103,22 @@ struct TsmArgs {
   void* k;
 };
 hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream);
+
+// Patch Selection Module: parameter count and workspace carving.
+struct PsmLayout {
+  size_t layer_params, params;
+  size_t h_off, x_off, q_off, k_off, v_off, att_off, ff_off, cu_off, total;
+};
+PsmLayout psm_layout(int B, int T, int d, int d_ff, int n_views, int n_layers);
+
+struct PsmArgs {
+  int B, T, d, n_heads, d_ff, n_views, n_layers;
+  const float* emb;
+  const float* params;
+  float* view_logit;
+  void* workspace;
+};
+hipError_t launch_psm_forward(const PsmArgs& a, hipStream_t stream);
 hipError_t launch_tsm_fold_gain(const void* w, const float* gamma, void* w_out, int rows, int cols,
                                 hipStream_t stream);
 

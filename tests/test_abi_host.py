@@ -266,3 +266,27 @@ def test_gather_hidden_validation():
     assert gh(rb=48 * 256 * 16 + 16) == _abi.ERR_BAD_SHAPE
     assert gh(h=MIS) == _abi.ERR_MISALIGNED
     assert gh(ki=A + 2) == _abi.ERR_MISALIGNED
+
+
+def test_psm_validation():
+    lib = lv.load()
+    n = lib.litevlm_psm_param_count(256, 1024, 6, 4)
+    per_layer = 4 * 256 + 3 * 256 * 256 + 3 * 256 + 256 * 256 + 256 + 1024 * 256 + 1024 + 256 * 1024 + 256
+    assert n == 4 * per_layer + 2 * 256 + 6 * 256 + 3 * (256 * 256 + 256) + 6 * 256 + 6
+    assert lib.litevlm_psm_workspace(1, 128, 256, 4, 1024) > 0
+    assert lib.litevlm_psm_workspace(1, 128, 200, 4, 1024) == 0
+
+    def pf(B=1, T=128, d=256, H=4, dff=1024, N=6, L=4, e=A, p=A, npar=None, o=A, ws=A, wsb=None):
+        npar = lib.litevlm_psm_param_count(d, dff, N, L) if npar is None else npar
+        wsb = lib.litevlm_psm_workspace(B, T, d, H, dff) if wsb is None else wsb
+        return lib.litevlm_psm_forward(B, T, d, H, dff, N, L, e, p, npar, o, ws, wsb, None)
+    assert pf(e=None) == _abi.ERR_NULL_POINTER
+    assert pf(o=None) == _abi.ERR_NULL_POINTER
+    assert pf(d=128, wsb=1 << 30) == _abi.ERR_BAD_SHAPE
+    assert pf(H=8) == _abi.ERR_UNSUPPORTED                     # head dim 32
+    assert pf(dff=1000, wsb=1 << 30) == _abi.ERR_BAD_SHAPE
+    assert pf(N=0) == _abi.ERR_BAD_SHAPE
+    assert pf(npar=5) == _abi.ERR_BAD_SHAPE
+    assert pf(p=A + 4) == _abi.ERR_MISALIGNED
+    assert pf(ws=None) == _abi.ERR_WORKSPACE
+    assert pf(wsb=100) == _abi.ERR_WORKSPACE
