@@ -430,7 +430,7 @@ def main():
         return {"workload": label, "layers": L, "tokens": T, "width": d, "heads": H, "d_ff": dff, "views": N,
                 "graph_us": round(graph_us, 2), "eager_us": round(eager_us, 2), "gflop": round(fl / 1e9, 3),
                 "tflops_graph": round(fl / (graph_us * 1e-6) / 1e12, 2),
-                "note": "32 dependent launches of a small network: latency-bound, reported for completeness"}
+                "note": "23 dependent launches of a small network: latency-bound, reported for completeness"}
 
     if args.workload == 3:
         main_runner = Runner([synth.config_case(3, run=run) for run in range(args.sets)])

@@ -107,7 +107,7 @@ hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream);
 // Patch Selection Module: parameter count and workspace carving.
 struct PsmLayout {
   size_t layer_params, params;
-  size_t h_off, x_off, q_off, k_off, v_off, att_off, ff_off, cu_off, total;
+  size_t h_off, q_off, k_off, v_off, att_off, ff_off, cu_off, total;
 };
 PsmLayout psm_layout(int B, int T, int d, int d_ff, int n_views, int n_layers);
 

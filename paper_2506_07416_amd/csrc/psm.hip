@@ -5,17 +5,15 @@
 // selection fuses with its lexical scores.
 //
 // The module is tiny (d = 256, 4 layers, 128 tokens at the benchmark shape),
-// so every step is latency-bound: the kernels favour few dependent global
-// round trips over peak rates.
-//   - psm_ln_kernel: LayerNorm, one wave per row (fp32 math, bf16 out); the
-//     first call also copies the embeddings into the fp32 residual stream and
-//     writes the per-sample row offsets the attention call reads.
-//   - psm_gemm_kernel: bf16 MFMA (v_mfma_f32_32x32x16_bf16) on x [M, K] times
+// so every step is latency-bound: the kernels favour few launches and few
+// dependent global round trips over peak rates.
+//   - psm_gemm_kernel: bf16 MFMA (v_mfma_f32_32x32x16_bf16) on A [M, K] times
 //     W^T, W [N, K] fp32 from the parameter vector (rounded to bf16 as it is
-//     loaded), with the bias and either a bf16 output (split into equal column
-//     ranges, for Q/K/V), GELU, or an add into the fp32 residual stream. A wave
-//     owns a 32 x 32 output block and reads its operands straight from global
-//     memory (the weights are re-read from L2 by the few row blocks).
+//     loaded). A workgroup owns one 32 x 32 output block and splits the k range
+//     over its 4 waves (more workgroups, fewer round trips each); A is either
+//     bf16 or the LayerNorm of fp32 rows formed as the operands load (the norm
+//     needs no launch of its own). Epilogues: bias plus a split bf16 output
+//     (Q/K/V), GELU, or an add into the fp32 residual stream.
 //   - self-attention: the library's prefill attention kernel, non-causal.
 //   - psm_cross_kernel: per (view, sample): the latent's query, its softmax over
 //     the encoded tokens, the attended value and the view's head.
@@ -31,98 +29,108 @@ __device__ __forceinline__ int psm_acc_row(int r, int hl) { return 8 * (r >> 2) 
 
 __device__ __forceinline__ float gelu_erf(float x) { return 0.5f * x * (1.f + erff(x * 0.7071067811865476f)); }
 
-// LayerNorm of one row per wave: y = (x - mean) / sqrt(var + 1e-5) * g + b.
-template <int EPL>
-__global__ __launch_bounds__(256) void psm_ln_kernel(const float* __restrict__ init, float* __restrict__ h,
-                                                     const float* __restrict__ g, const float* __restrict__ bta,
-                                                     uint16_t* __restrict__ y, int M, int B, int T,
-                                                     int32_t* __restrict__ cu) {
-  constexpr int d = EPL * kWave;
-  const int lane = threadIdx.x & 63;
-  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (cu && blockIdx.x == 0)
-    for (int t = threadIdx.x; t <= B; t += 256) cu[t] = t * T;
-  if (row >= M) return;
-  float x[EPL];
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    const size_t i = (size_t)row * d + lane + kWave * e;
-    x[e] = init ? init[i] : h[i];
-    if (init) h[i] = x[e];
-  }
-  float s = 0.f;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) s += x[e];
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) s += __shfl_xor(s, m, kWave);
-  const float mu = s / d;
-  float v = 0.f;
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) v = fmaf(x[e] - mu, x[e] - mu, v);
-#pragma unroll
-  for (int m = 1; m < kWave; m <<= 1) v += __shfl_xor(v, m, kWave);
-  const float r = 1.f / sqrtf(v / d + 1e-5f);
-#pragma unroll
-  for (int e = 0; e < EPL; ++e) {
-    const int c = lane + kWave * e;
-    y[(size_t)row * d + c] = f32_to_bf16_bits((x[e] - mu) * r * g[c] + bta[c]);
-  }
-}
-
 enum { kOutBf16 = 0, kOutGelu = 1, kOutResid = 2 };
 
-// out = x W^T + bias over a 64 x 64 tile per workgroup (2 x 2 waves of 32 x 32).
-// kOutBf16: columns split into nsplit equal ranges, range j to out[j] [M, N/nsplit];
-// kOutGelu: bf16 gelu(.) to out[0] [M, N]; kOutResid: h [M, N] += (.).
-template <int MODE>
-__global__ __launch_bounds__(256) void psm_gemm_kernel(const uint16_t* __restrict__ x, const float* __restrict__ W,
-                                                       const float* __restrict__ bias, int M, int N, int K,
-                                                       uint16_t* out0, uint16_t* out1, uint16_t* out2, int nsplit,
-                                                       float* __restrict__ h) {
+// out = A W^T + bias for one 32 x 32 output block per workgroup, the k range
+// split over its 4 waves (wave w: columns [w*K/4, (w+1)*K/4)) and the partial
+// blocks summed through LDS in wave order. A is either bf16 x [M, K] or, with
+// LNIN, the LayerNorm of the fp32 rows src [M, K] (gain g, bias bt, eps 1e-5),
+// formed as the operands load; every wave first takes the mean and variance of
+// the block's 32 rows (lane l32 / half hl: half hl of row l32).
+// Output: kOutBf16 columns split into nsplit equal ranges, range j to out[j]
+// [M, N/nsplit]; kOutGelu bf16 gelu(.) to out[0] [M, N]; kOutResid
+// h [M, N] = (rsrc ? rsrc : h) + (.). The block at (0, 0) also writes the
+// per-sample row offsets cu[t] = t*T (t <= B) when cu is given.
+template <int MODE, bool LNIN>
+__global__ __launch_bounds__(256) void psm_gemm_kernel(const uint16_t* __restrict__ x, const float* __restrict__ src,
+                                                       const float* __restrict__ g, const float* __restrict__ bt,
+                                                       const float* __restrict__ W, const float* __restrict__ bias,
+                                                       int M, int N, int K, uint16_t* out0, uint16_t* out1,
+                                                       uint16_t* out2, int nsplit, float* h,
+                                                       const float* __restrict__ rsrc, int32_t* cu, int B, int T) {
+  __shared__ float red[4][16][kWave];
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int l32 = lane & 31, hl = lane >> 5;
-  const int m0 = blockIdx.x * 64 + 32 * (w & 1), n0 = blockIdx.y * 64 + 32 * (w >> 1);
+  const int m0 = blockIdx.x * 32, n0 = blockIdx.y * 32;
+  if (cu && blockIdx.x == 0 && blockIdx.y == 0)
+    for (int t = threadIdx.x; t <= B; t += 256) cu[t] = t * T;
   const int arow = min(m0 + l32, M - 1);
-  const uint16_t* ap = x + (size_t)arow * K + 8 * hl;
-  const float* bp = W + (size_t)(n0 + l32) * K + 8 * hl;
+  float mu = 0.f, rstd = 1.f;
+  if constexpr (LNIN) {
+    const float4* rp = reinterpret_cast<const float4*>(src + (size_t)arow * K) + hl * (K / 8);
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll 8
+    for (int i = 0; i < K / 8; ++i) {
+      const float4 v = rp[i];
+      s1 += (v.x + v.y) + (v.z + v.w);
+      s2 = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, s2))));
+    }
+    s1 = sum_xor32(s1);
+    s2 = sum_xor32(s2);
+    mu = s1 / K;
+    rstd = 1.f / sqrtf(fmaxf(s2 / K - mu * mu, 0.f) + 1e-5f);
+  }
+  const int kw = K / 4, kbeg = w * kw;
+  const float* bp = W + (size_t)(n0 + l32) * K + kbeg + 8 * hl;
+  auto a_op = [&](int k) __attribute__((always_inline)) {
+    if constexpr (LNIN) {
+      const int c = kbeg + k + 8 * hl;
+      const float* xr = src + (size_t)arow * K + c;
+      const float4 x0 = *reinterpret_cast<const float4*>(xr), x1 = *reinterpret_cast<const float4*>(xr + 4);
+      const float4 g0 = *reinterpret_cast<const float4*>(g + c), g1 = *reinterpret_cast<const float4*>(g + c + 4);
+      const float4 b0 = *reinterpret_cast<const float4*>(bt + c), b1 = *reinterpret_cast<const float4*>(bt + c + 4);
+      const float y[8] = {(x0.x - mu) * rstd * g0.x + b0.x, (x0.y - mu) * rstd * g0.y + b0.y,
+                          (x0.z - mu) * rstd * g0.z + b0.z, (x0.w - mu) * rstd * g0.w + b0.w,
+                          (x1.x - mu) * rstd * g1.x + b1.x, (x1.y - mu) * rstd * g1.y + b1.y,
+                          (x1.z - mu) * rstd * g1.z + b1.z, (x1.w - mu) * rstd * g1.w + b1.w};
+      return pack_bf16x8(y);
+    } else {
+      return __builtin_bit_cast(bf16x8, *reinterpret_cast<const psm_u32x4*>(x + (size_t)arow * K + kbeg + k + 8 * hl));
+    }
+  };
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  // Chunks of CH k16 steps: every load of a chunk is issued before its MFMAs,
-  // so a chunk costs one memory round trip instead of CH.
-  constexpr int CH = 8;
+  // chunks of CH k16 steps: the chunk's loads are issued before its MFMAs
+  constexpr int CH = 4;
   int k = 0;
-  for (; k + 16 * CH <= K; k += 16 * CH) {
-    psm_u32x4 av[CH];
+  for (; k + 16 * CH <= kw; k += 16 * CH) {
+    bf16x8 av[CH];
     float4 bv0[CH], bv1[CH];
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      av[c] = *reinterpret_cast<const psm_u32x4*>(ap + k + 16 * c);
+      av[c] = a_op(k + 16 * c);
       bv0[c] = *reinterpret_cast<const float4*>(bp + k + 16 * c);
       bv1[c] = *reinterpret_cast<const float4*>(bp + k + 16 * c + 4);
     }
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
       const float bv[8] = {bv0[c].x, bv0[c].y, bv0[c].z, bv0[c].w, bv1[c].x, bv1[c].y, bv1[c].z, bv1[c].w};
-      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[c]), pack_bf16x8(bv), acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av[c], pack_bf16x8(bv), acc, 0, 0, 0);
     }
   }
-  for (; k < K; k += 16) {
-    const bf16x8 a = __builtin_bit_cast(bf16x8, *reinterpret_cast<const psm_u32x4*>(ap + k));
+  for (; k < kw; k += 16) {
+    const bf16x8 a = a_op(k);
     const float4 b0 = *reinterpret_cast<const float4*>(bp + k);
     const float4 b1 = *reinterpret_cast<const float4*>(bp + k + 4);
     const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
     acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pack_bf16x8(bv), acc, 0, 0, 0);
   }
+#pragma unroll
+  for (int r = 0; r < 16; ++r) red[w][r][lane] = acc[r];
+  __syncthreads();
+  // wave w finishes accumulator registers 4w .. 4w+3 of the block
   const int col = n0 + l32;
   const float bc = bias[col];
 #pragma unroll
-  for (int r = 0; r < 16; ++r) {
+  for (int rr = 0; rr < 4; ++rr) {
+    const int r = 4 * w + rr;
     const int row = m0 + psm_acc_row(r, hl);
+    const float val = (((red[0][r][lane] + red[1][r][lane]) + red[2][r][lane]) + red[3][r][lane]) + bc;
     if (row >= M) continue;
-    const float val = acc[r] + bc;
     if constexpr (MODE == kOutResid) {
-      h[(size_t)row * N + col] += val;
+      const size_t i = (size_t)row * N + col;
+      h[i] = (rsrc ? rsrc[i] : h[i]) + val;
     } else if constexpr (MODE == kOutGelu) {
       out0[(size_t)row * N + col] = f32_to_bf16_bits(gelu_erf(val));
     } else {
@@ -205,26 +213,19 @@ __global__ __launch_bounds__(256) void psm_cross_kernel(const uint16_t* __restri
   if (tid == 0) logit[(size_t)b * n_views + v] = ((red[0] + red[1]) + red[2]) + red[3] + b_head[v];
 }
 
-template <int EPL>
-void ln(const float* init, float* h, const float* g, const float* bt, uint16_t* y, int M, int B, int T, int32_t* cu,
-        hipStream_t s) {
-  hipLaunchKernelGGL((psm_ln_kernel<EPL>), dim3((M + 3) / 4), dim3(256), 0, s, init, h, g, bt, y, M, B, T, cu);
+template <int MODE, bool LNIN>
+void gemm(const uint16_t* x, const float* src, const float* g, const float* bt, const float* W, const float* bias,
+          int M, int N, int K, uint16_t* o0, uint16_t* o1, uint16_t* o2, int nsplit, float* h, const float* rsrc,
+          int32_t* cu, int B, int T, hipStream_t s) {
+  hipLaunchKernelGGL((psm_gemm_kernel<MODE, LNIN>), dim3((M + 31) / 32, N / 32), dim3(256), 0, s, x, src, g, bt, W,
+                     bias, M, N, K, o0, o1, o2, nsplit, h, rsrc, cu, B, T);
 }
 
-template <int MODE>
-void gemm(const uint16_t* x, const float* W, const float* bias, int M, int N, int K, uint16_t* o0, uint16_t* o1,
-          uint16_t* o2, int nsplit, float* h, hipStream_t s) {
-  hipLaunchKernelGGL((psm_gemm_kernel<MODE>), dim3((M + 63) / 64, N / 64), dim3(256), 0, s, x, W, bias, M, N, K, o0,
-                     o1, o2, nsplit, h);
-}
-
-template <int EPL>
 hipError_t run(const PsmArgs& a, hipStream_t s) {
   const PsmLayout L = psm_layout(a.B, a.T, a.d, a.d_ff, a.n_views, a.n_layers);
-  const int M = a.B * a.T, d = a.d, dff = a.d_ff;
+  const int M = a.B * a.T, d = a.d, dff = a.d_ff, B = a.B, T = a.T;
   uint8_t* ws = static_cast<uint8_t*>(a.workspace);
   float* h = reinterpret_cast<float*>(ws + L.h_off);
-  uint16_t* xl = reinterpret_cast<uint16_t*>(ws + L.x_off);
   uint16_t* q = reinterpret_cast<uint16_t*>(ws + L.q_off);
   uint16_t* k = reinterpret_cast<uint16_t*>(ws + L.k_off);
   uint16_t* v = reinterpret_cast<uint16_t*>(ws + L.v_off);
@@ -246,16 +247,18 @@ hipError_t run(const PsmArgs& a, hipStream_t s) {
     const float* b_up = w_up + (size_t)dff * d;
     const float* w_dn = b_up + dff;
     const float* b_dn = w_dn + (size_t)d * dff;
-    ln<EPL>(i == 0 ? a.emb : nullptr, h, ln1_g, ln1_b, xl, M, a.B, a.T, i == 0 ? cu : nullptr, s);
-    gemm<kOutBf16>(xl, w_qkv, b_qkv, M, 3 * d, d, q, k, v, 3, nullptr, s);
+    // the first layer reads the embeddings; its first residual add seeds h
+    const float* hin = i == 0 ? a.emb : h;
+    gemm<kOutBf16, true>(nullptr, hin, ln1_g, ln1_b, w_qkv, b_qkv, M, 3 * d, d, q, k, v, 3, nullptr, nullptr,
+                         i == 0 ? cu : nullptr, B, T, s);
     AttnArgs at;
     at.in_dtype = LITEVLM_BF16;
     at.out_dtype = LITEVLM_BF16;
-    at.B = a.B;
+    at.B = B;
     at.Hq = a.n_heads;
     at.Hkv = a.n_heads;
     at.D = d / a.n_heads;
-    at.max_seqlen = a.T;
+    at.max_seqlen = T;
     at.causal = 0;
     at.q = q;
     at.k = k;
@@ -266,10 +269,12 @@ hipError_t run(const PsmArgs& a, hipStream_t s) {
     at.o = att;
     const hipError_t e = launch_prefill_attn(at, s);
     if (e != hipSuccess) return e;
-    gemm<kOutResid>(att, w_o, b_o, M, d, d, nullptr, nullptr, nullptr, 1, h, s);
-    ln<EPL>(nullptr, h, ln2_g, ln2_b, xl, M, a.B, a.T, nullptr, s);
-    gemm<kOutGelu>(xl, w_up, b_up, M, dff, d, ff, nullptr, nullptr, 1, nullptr, s);
-    gemm<kOutResid>(ff, w_dn, b_dn, M, d, dff, nullptr, nullptr, nullptr, 1, h, s);
+    gemm<kOutResid, false>(att, nullptr, nullptr, nullptr, w_o, b_o, M, d, d, nullptr, nullptr, nullptr, 1, h,
+                           i == 0 ? a.emb : nullptr, nullptr, B, T, s);
+    gemm<kOutGelu, true>(nullptr, h, ln2_g, ln2_b, w_up, b_up, M, dff, d, ff, nullptr, nullptr, 1, nullptr, nullptr,
+                         nullptr, B, T, s);
+    gemm<kOutResid, false>(ff, nullptr, nullptr, nullptr, w_dn, b_dn, M, d, dff, nullptr, nullptr, nullptr, 1, h,
+                           nullptr, nullptr, B, T, s);
   }
   const float* fp = P + (size_t)a.n_layers * L.layer_params;
   const float* lnf_g = fp;
@@ -283,16 +288,17 @@ hipError_t run(const PsmArgs& a, hipStream_t s) {
   const float* b_cv = w_cv + (size_t)d * d;
   const float* w_hd = b_cv + d;
   const float* b_hd = w_hd + (size_t)a.n_views * d;
-  ln<EPL>(nullptr, h, lnf_g, lnf_b, xl, M, a.B, a.T, nullptr, s);
-  gemm<kOutBf16>(xl, w_ck, b_ck, M, d, d, q, nullptr, nullptr, 1, nullptr, s);
-  gemm<kOutBf16>(xl, w_cv, b_cv, M, d, d, k, nullptr, nullptr, 1, nullptr, s);
-  const size_t pbytes = (size_t)a.T * sizeof(float);
+  gemm<kOutBf16, true>(nullptr, h, lnf_g, lnf_b, w_ck, b_ck, M, d, d, q, nullptr, nullptr, 1, nullptr, nullptr,
+                       nullptr, B, T, s);
+  gemm<kOutBf16, true>(nullptr, h, lnf_g, lnf_b, w_cv, b_cv, M, d, d, k, nullptr, nullptr, 1, nullptr, nullptr,
+                       nullptr, B, T, s);
+  const size_t pbytes = (size_t)T * sizeof(float);
   if (d == 512)
-    hipLaunchKernelGGL((psm_cross_kernel<2>), dim3(a.n_views, a.B), dim3(256), pbytes, s, q, k, lat, w_cq, b_cq, w_hd,
-                       b_hd, a.view_logit, a.T, a.n_views);
+    hipLaunchKernelGGL((psm_cross_kernel<2>), dim3(a.n_views, B), dim3(256), pbytes, s, q, k, lat, w_cq, b_cq, w_hd,
+                       b_hd, a.view_logit, T, a.n_views);
   else
-    hipLaunchKernelGGL((psm_cross_kernel<1>), dim3(a.n_views, a.B), dim3(256), pbytes, s, q, k, lat, w_cq, b_cq, w_hd,
-                       b_hd, a.view_logit, a.T, a.n_views);
+    hipLaunchKernelGGL((psm_cross_kernel<1>), dim3(a.n_views, B), dim3(256), pbytes, s, q, k, lat, w_cq, b_cq, w_hd,
+                       b_hd, a.view_logit, T, a.n_views);
   return hipGetLastError();
 }
 
@@ -309,8 +315,6 @@ PsmLayout psm_layout(int B, int T, int d, int d_ff, int n_views, int n_layers) {
   size_t off = 0;
   L.h_off = off;
   off = a256(off + M * d * 4);
-  L.x_off = off;
-  off = a256(off + M * d * 2);
   L.q_off = off;
   off = a256(off + M * d * 2);
   L.k_off = off;
@@ -327,9 +331,6 @@ PsmLayout psm_layout(int B, int T, int d, int d_ff, int n_views, int n_layers) {
   return L;
 }
 
-hipError_t launch_psm_forward(const PsmArgs& a, hipStream_t stream) {
-  if (a.d == 256) return run<4>(a, stream);
-  return run<8>(a, stream);
-}
+hipError_t launch_psm_forward(const PsmArgs& a, hipStream_t stream) { return run(a, stream); }
 
 }  // namespace litevlm
