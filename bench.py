@@ -268,6 +268,18 @@ def main():
             del graphs
             return ms
 
+    def oracle_ms(fn, budget_s=3.0):
+        """Median wall time of the CPU oracle call fn() (at least one run, about
+        budget_s seconds), in ms; None when the CPU baselines are skipped."""
+        if args.no_cpu_baseline:
+            return None
+        runs, t_begin = [], time.perf_counter()
+        while not runs or (time.perf_counter() - t_begin < budget_s and len(runs) < 20):
+            t0 = time.perf_counter()
+            fn()
+            runs.append(time.perf_counter() - t0)
+        return round(float(np.median(runs)) * 1e3, 2)
+
     def measure_decode(runner, r, label, iters=200, warmup=5):
         """One extend-one decode step (litevlm_decode_attn) per sample over the
         compacted KV cache that the runner's last step left, after a step at keep
@@ -287,6 +299,7 @@ def main():
         scales = (c.q_scale, c.k_scale, c.v_scale)
         q1, k1, v1, scales = synth.decode_token_inputs(c.B, c.Hq, c.Hkv, c.D, c.dtype, seed=77,
                                                        scales=scales)
+        q1_h, k1_h, v1_h = q1, k1, v1
         t = runner.outs["kc"].dtype
         q1, k1, v1 = (up(x, c.dtype) for x in (q1, k1, v1))
         ws = torch.empty((lv.decode_workspace_bytes(t, c.B, c.Hq, c.Hkv, c.D, c.S),), dtype=torch.uint8,
@@ -325,7 +338,21 @@ def main():
         moved = cache_bytes + c.B * (c.Hq + 2 * c.Hkv) * c.D * e + c.B * c.Hq * c.D * 2
         del caches
         torch.cuda.empty_cache()
+        def dec_oracle():
+            import oracle
+            from oracle import litevlm as O
+            cache = [runner.outs[n][:total].cpu() for n in ("kc", "vc")]
+            bits = [t.view(torch.int16).numpy().view(np.uint16) if t.dtype == torch.bfloat16 else t.numpy()
+                    for t in cache]
+            sc = (c.q_scale, c.k_scale, c.v_scale)
+            dq = O.decode_stored(q1_h, c.dtype, sc[0])
+            dk, dv = O.decode_stored(k1_h, c.dtype, sc[1]), O.decode_stored(v1_h, c.dtype, sc[2])
+            oracle.decode_attention(dq, dk, dv, O.decode_stored(bits[0], c.dtype, sc[1]),
+                                    O.decode_stored(bits[1], c.dtype, sc[2]), cu_h, c.Hq, c.Hkv,
+                                    1.0 / math.sqrt(c.D))
+        cpu_ms = oracle_ms(dec_oracle)
         return {"workload": label, "dtype": c.dtype, "cache_len": np.diff(cu_h).tolist(),
+                "cpu_oracle_ms": cpu_ms,
                 "decode_us": round(us, 2), "cache_mb": round(cache_bytes / 1e6, 2),
                 "algorithmic_mb": round(moved / 1e6, 2), "gbs": round(moved / (us * 1e-6) / 1e9, 1),
                 "frac_hbm": round(moved / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
@@ -377,7 +404,16 @@ def main():
         kept = int(nv.sum().item()) + c.B * T
         fl_alg = 2.0 * Dm * (kept * c.Hkv * c.D + c.B * T * c.Hq * c.D)
         fl_done = 2.0 * Dm * (c.B * c.S * c.Hkv * c.D + c.B * T * c.Hq * c.D)
-        return {"workload": label, "model_width": Dm, "tsm_us": round(us, 2),
+        cpu_ms = None
+        if cfg == 3:
+            def tsm_oracle():
+                from oracle import litevlm as O
+                from oracle import tsm as OT
+                keep = tk.cpu().numpy()
+                OT.tsm_qk(O.decode_stored(hid, "bf16"), keep, c.V_full, gamma.astype(np.float64),
+                          O.decode_stored(wq, "bf16"), O.decode_stored(wk, "bf16"), c.Hq, c.Hkv, c.D, 1e-5, 1e6)
+            cpu_ms = oracle_ms(tsm_oracle, budget_s=1.0)
+        return {"workload": label, "model_width": Dm, "tsm_us": round(us, 2), "cpu_oracle_ms": cpu_ms,
                 "gflop_algorithmic": round(fl_alg / 1e9, 2), "gflop_computed": round(fl_done / 1e9, 2),
                 "tflops": round(fl_alg / (us * 1e-6) / 1e12, 1),
                 "frac_bf16_peak": round(fl_alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
@@ -427,7 +463,12 @@ def main():
         M = B * T
         fl = L * (2.0 * M * (3 * d * d + d * d + 2 * d * dff) + 4.0 * B * T * T * d) + 2.0 * M * 2 * d * d \
             + B * N * (2.0 * d * d + 4.0 * T * d)
+        def psm_oracle():
+            from oracle import psm as OP
+            OP.psm_forward(emb.astype(np.float64), par.astype(np.float64), H, dff, N, L)
+        cpu_ms = oracle_ms(psm_oracle, budget_s=2.0)
         return {"workload": label, "layers": L, "tokens": T, "width": d, "heads": H, "d_ff": dff, "views": N,
+                "cpu_oracle_ms": cpu_ms,
                 "graph_us": round(graph_us, 2), "eager_us": round(eager_us, 2), "gflop": round(fl / 1e9, 3),
                 "tflops_graph": round(fl / (graph_us * 1e-6) / 1e12, 2),
                 "note": "23 dependent launches of a small network: latency-bound, reported for completeness"}
