@@ -25,34 +25,35 @@
 // stages) were slower on both the batch-1 and the batch-8 shapes: the workgroups
 // wait on the copies, and what helps is more workgroups per CU, not deeper
 // rings.
+#include <type_traits>
+
 #include "common.hpp"
 #include "launch.hpp"
 
 namespace litevlm {
 namespace {
 
-// Tile shape (rows x output features) and ring depth; see the header comment.
-#ifndef TSM_MT
-#define TSM_MT 128
-#endif
-#ifndef TSM_NT
-#define TSM_NT 128
-#endif
-#ifndef TSM_STAGES
-#define TSM_STAGES 2
-#endif
-#ifndef TSM_KT
-#define TSM_KT 64
-#endif
-constexpr int kMT = TSM_MT, kNT = TSM_NT, kKT = TSM_KT, kStages = TSM_STAGES;  // Dm % kKT == 0 (host check)
+// Staging: 64 columns of the model width per stage, double buffered.
+constexpr int kKT = 64, kStages = 2;  // Dm % kKT == 0 (host check)
 constexpr int kPieces = kKT / 8;      // 16-byte pieces per staged row
 constexpr int kRowB = kKT * 2;        // bytes per staged row
-constexpr int kAB = kMT * kRowB;      // A tile bytes per stage
-constexpr int kBB = kNT * kRowB;      // B tile bytes per stage
-constexpr int kStageB = kAB + kBB;
-constexpr int kRingB = kStages * kStageB;
-constexpr int kLdsB = kRingB + kMT * 4 /* row factors */ + kMT * 4 /* positions */ + 64 /* reductions */;
-constexpr int kWgPerCu = (160 * 1024 / kLdsB) >= 4 ? 4 : (160 * 1024 / kLdsB) >= 1 ? 160 * 1024 / kLdsB : 1;
+
+// Workgroup tile MT rows x NT features over NW waves; each wave holds 64 rows
+// (two 32-row blocks) and NT / (NW / (MT / 64)) features.
+template <int MT, int NT, int NW>
+struct TsmTile {
+  static constexpr int kAB = MT * kRowB;  // A tile bytes per stage
+  static constexpr int kBB = NT * kRowB;  // B tile bytes per stage
+  static constexpr int kStageB = kAB + kBB;
+  static constexpr int kRingB = kStages * kStageB;
+  static constexpr int kLdsB = kRingB + MT * 4 /* row factors */ + MT * 4 /* positions */ + 128 /* reductions */;
+  static constexpr int kWgPerCu = (160 * 1024 / kLdsB) >= 2 ? 2 : 1;
+  static constexpr int kThreads = 64 * NW;
+  static constexpr int kNWR = MT / 64;       // waves along the rows
+  static constexpr int kNWC = NW / kNWR;     // waves along the features (share rows)
+  static constexpr int kCBW = NT / kNWC / 32;  // 32-feature blocks per wave
+  static_assert(kNWR * kNWC == NW && (kCBW == 2 || kCBW == 4), "tile shape");
+};
 
 struct TsmParams {
   const uint8_t* x;     // bf16 [B, S, Dm]
@@ -94,12 +95,14 @@ __device__ __forceinline__ float dot2_bf16(uint32_t x, uint32_t y, float c) {
   return __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2v, x), __builtin_bit_cast(bf16x2v, y), c, false);
 }
 
-template <int D>
-__global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
-  constexpr int PB = D / 64;       // column-block distance of rotary partners
-  constexpr int RB = kMT / 64;     // 32-row blocks per wave (waves split the rows in two)
-  constexpr int CBW = kNT / 64;    // 32-column blocks per wave (waves split the columns in two)
-  static_assert(CBW == 2 || CBW == 4, "tile width");
+template <int D, int MT, int NT, int NW>
+__global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_proj_kernel(TsmParams p) {
+  using Tl = TsmTile<MT, NT, NW>;
+  constexpr int kMT = MT, kNT = NT, kAB = Tl::kAB, kBB = Tl::kBB, kStageB = Tl::kStageB, kRingB = Tl::kRingB;
+  constexpr int kTh = Tl::kThreads, NWR = Tl::kNWR, NWC = Tl::kNWC;
+  constexpr int PB = D / 64;     // column-block distance of rotary partners
+  constexpr int RB = 2;          // 32-row blocks per wave
+  constexpr int CBW = Tl::kCBW;  // 32-column blocks per wave
   const int L = blockIdx.x;
   const int item = (L & 7) * p.per_xcd + (L >> 3);  // an XCD takes a contiguous item range
   if (item >= p.n_items) return;
@@ -126,26 +129,30 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
   const int H = isq ? p.Hq : p.Hkv;
   const int Dm = p.Dm;
 
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kLdsB];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tl::kLdsB];
   float* rs = reinterpret_cast<float*>(lds + kRingB);
   int* pos = reinterpret_cast<int*>(lds + kRingB + kMT * 4);
   int* red = reinterpret_cast<int*>(lds + kRingB + kMT * 8);
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int wr = w & 1, wc = w >> 1, hl = lane >> 5, l32 = lane & 31;
+  const int wr = w % NWR, wc = w / NWR, hl = lane >> 5, l32 = lane & 31;
 
   // ---- positions of the tile's rows in the patch-selected sequence
   {
     const uint8_t* kr = p.keep ? p.keep + (size_t)b * p.S : nullptr;
     int cnt = 0;
     if (kr)
-      for (int j = tid; j < row0; j += 256) cnt += kr[j];
+      for (int j = tid; j < row0; j += kTh) cnt += kr[j];
 #pragma unroll
     for (int x = 1; x < kWave; x <<= 1) cnt += __shfl_xor(cnt, x, kWave);
     if (lane == 0) red[w] = cnt;
     __syncthreads();
-    const int base = kr ? red[0] + red[1] + red[2] + red[3] : row0;
-    for (int t0 = 0; t0 < kMT; t0 += 256) {
+    int base = row0;
+    if (kr) {
+      base = 0;
+      for (int x = 0; x < NW; ++x) base += red[x];
+    }
+    for (int t0 = 0; t0 < kMT; t0 += kTh) {
       const int t = t0 + tid;
       int f = 0;
       if (t < nrows) f = kr ? kr[row0 + t] : 1;
@@ -156,29 +163,33 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
         if (lane >= x) incl += y;
       }
       __syncthreads();
-      if (lane == kWave - 1) red[4 + w] = incl;
+      if (lane == kWave - 1) red[NW + w] = incl;
       __syncthreads();
-      int before = t0 == 0 ? 0 : red[8];  // kept rows of the earlier chunks
-      for (int x = 0; x < w; ++x) before += red[4 + x];
+      int before = t0 == 0 ? 0 : red[2 * NW];  // kept rows of the earlier chunks
+      for (int x = 0; x < w; ++x) before += red[NW + x];
       if (t < kMT) pos[t] = base + before + (incl - f);
       __syncthreads();
-      if (tid == 0) red[8] = (t0 == 0 ? 0 : red[8]) + red[4] + red[5] + red[6] + red[7];
+      if (tid == 0) {
+        int c = t0 == 0 ? 0 : red[2 * NW];
+        for (int x = 0; x < NW; ++x) c += red[NW + x];
+        red[2 * NW] = c;
+      }
     }
   }
 
   // ---- per-lane copy sources (fixed) and operand offsets (fixed)
   // copy j of a wave fills LDS pieces (w + 4j)*64 + lane of the A (resp. B) tile
-  constexpr int CA = kAB / 4096, CB = kBB / 4096;  // copies per thread per stage
+  constexpr int CA = kAB / (1024 * NW), CB = kBB / (1024 * NW);  // copies per thread per stage
   size_t asrc[CA], bsrc[CB];
 #pragma unroll
   for (int j = 0; j < CA; ++j) {
-    const int slot = (w + 4 * j) * 64 + lane;
+    const int slot = (w + NW * j) * 64 + lane;
     const int row = slot / kPieces, logical = (slot % kPieces) ^ swz(row);
     asrc[j] = ((size_t)((size_t)b * p.S + row0 + min(row, nrows - 1)) * Dm + logical * 8) * 2;
   }
 #pragma unroll
   for (int j = 0; j < CB; ++j) {
-    const int slot = (w + 4 * j) * 64 + lane;
+    const int slot = (w + NW * j) * 64 + lane;
     const int row = slot / kPieces, logical = (slot % kPieces) ^ swz(row);
     bsrc[j] = ((size_t)(n0 + row) * Dm + logical * 8) * 2;
   }
@@ -188,7 +199,7 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
   if constexpr (CBW == 4) {
 #pragma unroll
     for (int i = 0; i < 4; ++i) cbl[i] = 4 * wc + i;
-  } else {
+  } else {  // two waves share a 128-feature span: blocks {c0, c0 + PB}
     cbl[0] = (D == 128) ? wc : 2 * wc;
     cbl[1] = cbl[0] + PB;
   }
@@ -199,7 +210,7 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
     const int logical = 2 * ks + hl;
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int row = (kMT / 2) * wr + 32 * rb + l32;
+      const int row = 64 * wr + 32 * rb + l32;
       aoff[rb][ks] = row * kRowB + ((logical ^ swz(row)) * 16);
     }
 #pragma unroll
@@ -215,11 +226,11 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
 #pragma unroll
     for (int j = 0; j < CA; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(p.x + asrc[j] + kb),
-                                       (__attribute__((address_space(3))) void*)(st + lds_w + 4 * j * 1024), 16, 0, 0);
+                                       (__attribute__((address_space(3))) void*)(st + lds_w + NW * j * 1024), 16, 0, 0);
 #pragma unroll
     for (int j = 0; j < CB; ++j)
       __builtin_amdgcn_global_load_lds((const void*)(W + bsrc[j] + kb),
-                                       (__attribute__((address_space(3))) void*)(st + kAB + lds_w + 4 * j * 1024), 16,
+                                       (__attribute__((address_space(3))) void*)(st + kAB + lds_w + NW * j * 1024), 16,
                                        0, 0);
   };
 
@@ -264,7 +275,7 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
       // Row sums of squares from the A operands on the packed bf16 dot unit. The
       // two waves holding the same rows take alternate k16 steps, so every SIMD
       // carries the same vector work.
-      if ((ks & 1) == wc) {
+      if ((ks % NWC) == wc) {
 #pragma unroll
         for (int rb = 0; rb < RB; ++rb) {
           const u32x4v u = __builtin_bit_cast(u32x4v, a[rb]);
@@ -277,31 +288,31 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
 
   // ---- epilogue: RMS factor per row, rotary embedding, bf16 store
   // (the ring is free now: its first bytes hold the wc = 1 waves' partial sums)
-  float* part = reinterpret_cast<float*>(lds);
+  float* part = reinterpret_cast<float*>(lds);  // [NWC][kMT]
   __syncthreads();
-  if (wc == 1) {
 #pragma unroll
-    for (int rb = 0; rb < RB; ++rb) {
-      const float tot = sum_xor32(ssq[rb]);
-      if (hl == 0) part[(kMT / 2) * wr + 32 * rb + l32] = tot;
-    }
+  for (int rb = 0; rb < RB; ++rb) {
+    const float tot = sum_xor32(ssq[rb]);
+    if (hl == 0) part[wc * kMT + 64 * wr + 32 * rb + l32] = tot;
   }
   __syncthreads();
-  if (wc == 0) {
+  if (wc == 0 && hl == 0) {
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb) {
-      const int row = (kMT / 2) * wr + 32 * rb + l32;
-      const float tot = sum_xor32(ssq[rb]);
-      if (hl == 0) rs[row] = 1.f / sqrtf((tot + part[row]) / (float)Dm + p.eps);
+      const int row = 64 * wr + 32 * rb + l32;
+      float tot = 0.f;
+      for (int x = 0; x < NWC; ++x) tot += part[x * kMT + row];
+      rs[row] = 1.f / sqrtf(tot / (float)Dm + p.eps);
     }
   }
   __syncthreads();
   uint16_t* out = isq ? p.q : p.k;
-#pragma unroll
-  for (int i = 0; i < CBW / 2; ++i) {
-    // slots c (a first-half block) and cp (its partner, PB blocks on) of this wave's list
-    const int c = CBW == 2 ? 0 : (D == 128 ? i : 2 * i);
-    const int cp = CBW == 2 ? 1 : c + PB;
+  // rotary pairs of this wave's column list: slots c (a first-half block) and
+  // cp (its partner, PB blocks on)
+  auto rotate_pair = [&](auto ic) __attribute__((always_inline)) {
+    constexpr int i = decltype(ic)::value;
+    constexpr int c = CBW == 2 ? 0 : (D == 128 ? i : 2 * i);
+    constexpr int cp = CBW == 2 ? 1 : c + PB;
     const int d = (32 * cbl[c]) % D + l32;  // element of the first half of its head (d < D/2)
     const int head = (n0 + 32 * cbl[c]) / D;
     const double inv_freq = exp2(-(2.0 * d / D) * p.log2_theta);
@@ -309,7 +320,7 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int row = (kMT / 2) * wr + 32 * rb + acc_row(r, hl);
+        const int row = 64 * wr + 32 * rb + acc_row(r, hl);
         if (row < nrows) {
           const float f = rs[row];
           const float x1 = acc[rb][c][r] * f, x2 = acc[rb][cp][r] * f;
@@ -323,7 +334,9 @@ __global__ __launch_bounds__(256, kWgPerCu) void tsm_proj_kernel(TsmParams p) {
           o[d + D / 2] = f32_to_bf16_bits(x2 * cs + x1 * sn);
         }
       }
-  }
+  };
+  rotate_pair(std::integral_constant<int, 0>{});
+  if constexpr (CBW == 4) rotate_pair(std::integral_constant<int, 1>{});
 }
 
 // w_out[n, c] = bf16(w[n, c] * gamma[c]): the RMS normalisation gain folded
@@ -352,19 +365,32 @@ hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream) {
   p.Dm = a.Dm;
   p.Hq = a.Hq;
   p.Hkv = a.Hkv;
-  const int T = a.S - a.V_full;
-  p.mk = (a.S + kMT - 1) / kMT;
-  p.nk = a.Hkv * a.D / kNT;
-  p.mq = (T + kMT - 1) / kMT;
-  p.nq = a.Hq * a.D / kNT;
-  p.n_k_items = a.B * p.mk * p.nk;
-  p.n_items = p.n_k_items + a.B * p.mq * p.nq;
-  p.per_xcd = (p.n_items + 7) / 8;
   p.eps = a.eps;
   p.log2_theta = log2((double)a.rope_theta);
-  const dim3 grid(8 * p.per_xcd);
-  if (a.D == 128) hipLaunchKernelGGL((tsm_proj_kernel<128>), grid, dim3(256), 0, stream, p);
-  else hipLaunchKernelGGL((tsm_proj_kernel<64>), grid, dim3(256), 0, stream, p);
+  const int T = a.S - a.V_full;
+  auto setup = [&](int MT, int NT) {
+    p.mk = (a.S + MT - 1) / MT;
+    p.nk = a.Hkv * a.D / NT;
+    p.mq = (T + MT - 1) / MT;
+    p.nq = a.Hq * a.D / NT;
+    p.n_k_items = a.B * p.mk * p.nk;
+    p.n_items = p.n_k_items + a.B * p.mq * p.nq;
+    p.per_xcd = (p.n_items + 7) / 8;
+    return dim3(8 * p.per_xcd);
+  };
+  // 256 x 256 tiles (8 waves, one workgroup per CU) halve the L2 traffic per
+  // flop; they are used when they still give every CU a workgroup.
+  const bool big = (a.Hkv * a.D) % 256 == 0 && (a.Hq * a.D) % 256 == 0 &&
+                   (int64_t)a.B * ((a.S + 255) / 256) * (a.Hkv * a.D / 256) >= 256;
+  if (big) {
+    const dim3 grid = setup(256, 256);
+    if (a.D == 128) hipLaunchKernelGGL((tsm_proj_kernel<128, 256, 256, 8>), grid, dim3(512), 0, stream, p);
+    else hipLaunchKernelGGL((tsm_proj_kernel<64, 256, 256, 8>), grid, dim3(512), 0, stream, p);
+  } else {
+    const dim3 grid = setup(128, 128);
+    if (a.D == 128) hipLaunchKernelGGL((tsm_proj_kernel<128, 128, 128, 4>), grid, dim3(256), 0, stream, p);
+    else hipLaunchKernelGGL((tsm_proj_kernel<64, 128, 128, 4>), grid, dim3(256), 0, stream, p);
+  }
   return hipGetLastError();
 }
 
