@@ -32,7 +32,11 @@ PEAK_FP8_TFLOPS = 5000.0
 PEAK_HBM_GBS = 8000.0
 HEADLINE_R = 0.5
 SWEEP = (1.0, 0.5, 0.25)
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attn_bf16_cfg3_traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_cfg3_keep050.json")
+CSRC = os.path.join(ROOT, "paper_2506_07416_amd", "csrc")
+# source file of each kernel family, for keying counter figures to the code they measured
+KERNEL_SOURCES = (("attn_", "attn.hip"), ("score_", "score.hip"), ("topk_", "score.hip"),
+                  ("gather_rows", "score.hip"), ("patch_select", "patch_select.hip"))
 
 
 def parse():
@@ -42,6 +46,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--sets", type=int, default=4, help="rotating input sets (cold-cache)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--settle-s", type=float, default=0.3,
+                    help="seconds of untimed back-to-back steps before the timed region (clock settle)")
     ap.add_argument("--no-sweep", action="store_true")
     ap.add_argument("--keep-ratio", type=float, default=None,
                     help="keep ratio of the timed workload (default 0.5 for the 6x1024 workload, "
@@ -49,6 +55,16 @@ def parse():
     ap.add_argument("--workload", type=int, default=3, choices=(3, 4, 5),
                     help="3: 6x1024+128 batch 1 bf16 (the reported line); 4/5: batch-8 ragged bf16/fp8, "
                          "for profiling")
+    ap.add_argument("--traffic-calibrate", type=float, metavar="MB", default=None,
+                    help="run only a plain fp32 copy of MB megabytes (read, and the same written) 5 times: "
+                         "profiled with --pmc FETCH_SIZE and then WRITE_SIZE it calibrates the counters")
+    ap.add_argument("--traffic-reduce", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                          "COPY_WRITE_CSV"), default=None,
+                    help="reduce four rocprofv3 counter_collection.csv files (the step's FETCH_SIZE and "
+                         "WRITE_SIZE runs, the calibration copy's) into per-kernel HBM bytes per launch, "
+                         "written to --traffic-out")
+    ap.add_argument("--copy-mb", type=float, default=256.0, help="size of the calibration copy (MB)")
+    ap.add_argument("--traffic-out", default=TRAFFIC_FILE)
     return ap.parse_args()
 
 
@@ -69,6 +85,114 @@ def gather_bytes(seqlens, Hq, Hkv, D, e):
 def source_hash(path):
     with open(path, "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def kernel_source(name):
+    for prefix, src in KERNEL_SOURCES:
+        if name.startswith(prefix):
+            return src
+    return None
+
+
+def max_len_bound(r, V_full, T):
+    """Host bound on every compacted length at keep ratio r, known without a
+    device sync: at most floor(r*V_full + 1e-6) visual tokens survive (V_b <=
+    V_full) and every text token does. It sizes the attention grid."""
+    return min(V_full, int(math.floor(r * V_full + 1e-6))) + T
+
+
+def traffic_calibrate(mb):
+    import torch
+    n = int(mb * 1e6) // 4
+    x = torch.ones(n, dtype=torch.float32, device="cuda")
+    y = torch.empty_like(x)
+    for _ in range(5):
+        torch.add(x, 0.0, out=y)
+    torch.cuda.synchronize()
+    print(f"copy: {n * 4} bytes read and {n * 4} written per launch, 5 launches", flush=True)
+
+
+def _per_dispatch(path, counter):
+    """{kernel name: median over dispatches of counter (KiB)} from a rocprofv3
+    counter_collection.csv (values of one dispatch summed over its rows)."""
+    import csv
+    from statistics import median
+    vals = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter:
+            continue
+        key = (r["Kernel_Name"], r.get("Dispatch_Id") or r.get("Correlation_Id"))
+        vals[key] = vals.get(key, 0.0) + float(r["Counter_Value"])
+    per = {}
+    for (name, _), v in vals.items():
+        per.setdefault(name, []).append(v)
+    return {k: (median(v), len(v)) for k, v in per.items()}
+
+
+def traffic_reduce(fa, wa, fc, wc, mb, out):
+    """HBM bytes per launch of every kernel in the step's counter runs: each
+    counter scaled by (known bytes / measured) of the calibration copy."""
+    known = int(mb * 1e6) // 4 * 4
+    fetch, write = _per_dispatch(fa, "FETCH_SIZE"), _per_dispatch(wa, "WRITE_SIZE")
+    cf = [v for k, v in _per_dispatch(fc, "FETCH_SIZE").items() if "elementwise" in k]
+    cw = [v for k, v in _per_dispatch(wc, "WRITE_SIZE").items() if "elementwise" in k]
+    if not cf or not cw:
+        raise SystemExit("no elementwise copy dispatches in the calibration files")
+    kf = known / (cf[0][0] * 1024.0)
+    kw = known / (cw[0][0] * 1024.0)
+    rec = {"copy_known_bytes": known, "copy_fetch_kib": cf[0][0], "copy_write_kib": cw[0][0],
+           "fetch_scale": kf, "write_scale": kw, "kernels": {}}
+    for name in sorted(set(fetch) & set(write)):
+        src = kernel_source(name)
+        if src is None:
+            continue
+        f_kib, n_f = fetch[name]
+        w_kib, n_w = write[name]
+        rec["kernels"][name] = {
+            "fetch_kib_per_dispatch": f_kib, "write_kib_per_dispatch": w_kib, "dispatches": [n_f, n_w],
+            "hbm_bytes_per_launch": round(f_kib * 1024.0 * kf + w_kib * 1024.0 * kw),
+            "source": src, "source_sha256_16": source_hash(os.path.join(CSRC, src))}
+    with open(out, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec, indent=1))
+
+
+def measured_traffic(prefix):
+    """HBM bytes per launch of the first kernel whose name starts with prefix,
+    from the counter file, or None when absent or when its source file has
+    changed since the counters were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as f:
+        tr = json.load(f)
+    for name, k in tr.get("kernels", {}).items():
+        if name.startswith(prefix):
+            if k.get("source_sha256_16") == source_hash(os.path.join(CSRC, k["source"])):
+                return k["hbm_bytes_per_launch"]
+            return None
+    return None
+
+
+def host_description():
+    """CPU model and NumPy's BLAS build, for the CPU baseline."""
+    import numpy as np
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = None
+    try:
+        cfg = np.show_config(mode="dicts")
+        b = cfg["Build Dependencies"]["blas"]
+        blas = f"{b.get('name')} {b.get('version')}"
+    except Exception:  # pragma: no cover
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "numpy": np.__version__, "blas": blas}
 
 
 def cpu_baseline(case, r, budget_s=10.0):
@@ -103,6 +227,7 @@ def cpu_baseline(case, r, budget_s=10.0):
     t_sel = median(a for a, _ in runs)
     t_att = median(b for _, b in runs)
     return {"value": round(med * 1e3, 1), "unit": "ms", "cores": int(cores), "kind": "oracle",
+            "host": host_description(),
             "sample": f"the whole step on the same inputs, {len(runs)} runs in {sum(tot):.1f} s "
                       f"(median run: selection stage {t_sel:.2f} s, gather + attention over all "
                       f"{int(res['cu_seqlens'][-1])} query rows {t_att:.2f} s)"}
@@ -154,6 +279,12 @@ def clocks_under_load(run_steps, seconds=1.0):
 
 def main():
     args = parse()
+    if args.traffic_reduce is not None:
+        traffic_reduce(*args.traffic_reduce, args.copy_mb, args.traffic_out)
+        return
+    if args.traffic_calibrate is not None:
+        traffic_calibrate(args.traffic_calibrate)
+        return
     if args.gpus != 1:
         print(f"bench.py runs on exactly one GPU; --gpus {args.gpus} is not supported "
               "(the path has no multi-GPU mode in this build).", file=sys.stderr)
@@ -208,8 +339,8 @@ def main():
             if ev is not None:
                 ev[2].record(stream)
             lv.prefill_attn(self.outs["qc"], self.outs["kc"], self.outs["vc"], self.outs["cu_seqlens"],
-                            c.S, B=c.B, q_scale=c.q_scale, k_scale=c.k_scale, v_scale=c.v_scale,
-                            out=self.o)
+                            max_len_bound(r, c.V_full, c.S - c.V_full), B=c.B, q_scale=c.q_scale,
+                            k_scale=c.k_scale, v_scale=c.v_scale, out=self.o)
             if ev is not None:
                 ev[3].record(stream)
 
@@ -486,7 +617,7 @@ def main():
     # Clock settle: the step back to back for about 0.3 s before any timed
     # region, so the headline is taken at the GPU's steady clocks (untimed).
     t_settle = time.perf_counter()
-    while time.perf_counter() - t_settle < 0.3:
+    while time.perf_counter() - t_settle < args.settle_s:
         for i in range(20):
             main_runner.step(main_runner.sets[i % len(main_runner.sets)], args.keep_ratio)
         torch.cuda.synchronize()
@@ -497,17 +628,19 @@ def main():
     fl = attn_flops(seqlens, Hq, D)
     attn_us = per[2] * 1e3
     attn_tflops = fl / (attn_us * 1e-6) / 1e12
-    V_b = [V] * B
+    esz = {"f32": 4, "bf16": 2, "fp8": 1}[case.dtype]
+    V_b = [V - len(m) * case.Tv for m in case.masked_views]
     sel_flops = score_flops(V_b, T, Hq, D)
-    gbytes = gather_bytes(seqlens, Hq, Hkv, D, 2)
-
-    traffic = None
-    if os.path.exists(TRAFFIC_FILE):
-        with open(TRAFFIC_FILE) as f:
-            tr = json.load(f)
-        if tr.get("source_sha256_16") == source_hash(os.path.join(ROOT, "paper_2506_07416_amd", "csrc",
-                                                                  "attn.hip")):
-            traffic = tr.get("hbm_bytes_per_launch")
+    gbytes = gather_bytes(seqlens, Hq, Hkv, D, esz)
+    # algorithmic bytes of the select call: the text query rows and the kept
+    # keys read by the scoring, the token mask, the scores and packed indices
+    # written, and the gather's reads and writes
+    sel_bytes = (B * T * Hq * D * esz + sum(v + T for v in V_b) * Hkv * D * esz + B * S
+                 + 4 * B * V + 4 * sum(seqlens) + gbytes)
+    sel_us = per[1] * 1e3
+    traffic = measured_traffic("attn_bf16_kernel")
+    sel_traffic = {k: measured_traffic(k) for k in ("score_rowstats", "score_colmass", "topk_compact",
+                                                    "gather_rows")}
 
     sweep = []
     if not args.no_sweep:
@@ -585,8 +718,15 @@ def main():
         "kernels_us": {"patch_select": round(per[0] * 1e3, 2),
                        "token_score_topk_gather": round(per[1] * 1e3, 2),
                        "prefill_attn": round(attn_us, 2)},
-        "select_stage": {"score_gflop": round(sel_flops / 1e9, 3),
-                         "gather_mb": round(gbytes / 1e6, 2)},
+        "select_stage": {"call": "litevlm_token_score_topk (score sweeps, top-k, gather)", "bound": "hbm",
+                         "us": round(sel_us, 2), "algorithmic_bytes": sel_bytes,
+                         "achieved": round(sel_bytes / (sel_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
+                         "unit": "GB/s", "frac": round(sel_bytes / (sel_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                         "score_gflop": round(sel_flops / 1e9, 3),
+                         "score_tflops_over_call": round(sel_flops / (sel_us * 1e-6) / 1e12, 1),
+                         "gather_mb": round(gbytes / 1e6, 2),
+                         "traffic_per_kernel": sel_traffic,
+                         "note": "event-timed whole call; per-kernel durations and counters are in profiles/"},
         "roofline": {"bound": "mfma", "kernel": "attn_bf16_kernel",
                      "achieved": round(attn_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,

@@ -12,6 +12,7 @@ and brute force. No function is "parity unpinned".
 """
 from .litevlm import (  # noqa: F401
     decode_inputs,
+    view_scores,
     patch_select,
     token_keep_from_views,
     patch_selected_positions,

@@ -5,9 +5,7 @@ Resource-Constrained Environments" (arXiv 2506.07416). Only tests, the smoke
 check and the benchmark's CPU-baseline leg use this module.
 
 Each function restates the passage it follows and the reading taken where the
-paper is silent. Everything except the patch-selection threshold decision runs
-in float64 on the exact stored input values; that decision runs in float32,
-the precision the kernel takes it in.
+paper is silent. Everything runs in float64 on the exact stored input values.
 """
 from __future__ import annotations
 
@@ -44,29 +42,31 @@ def decode_inputs(case):
 
 # --------------------------------------------------------------------------- patch selection
 
+def view_scores(view_logit: np.ndarray, view_lexical: Optional[np.ndarray],
+                w_lexical: float) -> np.ndarray:
+    """Fused view score (Design section, Patch Selection Module paragraph: the
+    final score of a view is a weighted sum of the lexical mapping and the
+    module's logit). Reading: the logit enters through the logistic function
+    so that both terms live on [0, 1], s_v = w*lex_v + (1-w)*sigmoid(logit_v),
+    and a missing lexical term counts as 0. float64 throughout. Returns [B, N]."""
+    logit = np.asarray(view_logit, dtype=np.float64)
+    lex = np.zeros_like(logit) if view_lexical is None else np.asarray(view_lexical, np.float64)
+    w = float(w_lexical)
+    sig = 1.0 / (1.0 + np.exp(-logit))
+    return w * lex + (1.0 - w) * sig
+
+
 def patch_select(view_logit: np.ndarray, view_lexical: Optional[np.ndarray],
                  w_lexical: float, threshold: float) -> np.ndarray:
     """View selection at inference (Design section, Patch Selection Module
-    paragraph): the final view score is a weighted sum of the lexical mapping
-    and the module's logits, and views scoring above a threshold are kept.
-
-    Reading: the logit enters through the logistic function so that both terms
-    live on [0, 1]: s_v = w*lex_v + (1-w)*sigmoid(logit_v); a missing lexical
-    term counts as 0; "above" is strict (s_v > threshold); if no view passes,
-    the single best view is kept (lowest index among equal scores).
-
-    The comparison decides a boolean, so it runs in float32 like the kernel:
-    sigmoid(x) = 1/(1+exp(-x)), then w*lex, (1-w)*sigmoid and their sum, each
-    rounded to float32. Returns uint8 [B, N].
-    """
-    logit = np.asarray(view_logit, dtype=np.float32)
-    B, N = logit.shape
-    one = np.float32(1.0)
-    w = np.float32(w_lexical)
-    tau = np.float32(threshold)
-    sig = one / (one + np.exp(-logit))
-    lex = np.zeros_like(logit) if view_lexical is None else np.asarray(view_lexical, np.float32)
-    s = (w * lex).astype(np.float32) + ((one - w) * sig).astype(np.float32)
+    paragraph): views whose fused score (view_scores) lies above a threshold
+    are kept. Reading: "above" is strict (s_v > threshold); if no view passes,
+    the single best view is kept (lowest index among equal scores), since a
+    prompt needs at least one view. The decision is taken in float64 on the
+    float64 fused score. Returns uint8 [B, N]."""
+    s = view_scores(view_logit, view_lexical, w_lexical)
+    tau = float(threshold)
+    B, N = s.shape
     keep = np.zeros((B, N), np.uint8)
     for b in range(B):
         for v in range(N):

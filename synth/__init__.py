@@ -280,3 +280,42 @@ def psm_inputs(B: int, T: int, d: int, d_ff: int, n_views: int, n_layers: int, s
     weight(d, d), bias(d), weight(d, d), bias(d), weight(d, d), bias(d)
     weight(n_views, d), bias(n_views)
     return emb, np.concatenate(segs).astype(np.float32)
+
+
+def with_zero_queries(case: Case) -> Case:
+    """A copy of ``case`` whose queries are all zero (stored bits 0 encode +0.0
+    in every dtype): every attention row is then uniform over its visible keys."""
+    return dataclasses.replace(case, q=np.zeros_like(case.q))
+
+
+def with_duplicated_keys(case: Case, b: int, members: Sequence[int], beta: float) -> Case:
+    """A copy of ``case`` in which the visual tokens ``members`` of sample b share
+    one key row (every KV head): the key of members[0] plus beta*sqrt(D)*u_g,
+    u_g the unit vector of the sum of KV group g's text queries (the "aligned"
+    plant, which lifts the group's attention above the other tokens). The row
+    is encoded once and its stored bits copied to every member, so the members'
+    keys are bitwise identical."""
+    G = case.Hq // case.Hkv
+    k = case.k.copy()
+    scale = case.k_scale
+    if case.dtype == F32:
+        qf = case.q[b].astype(np.float64)
+        kf = case.k[b, members[0]].astype(np.float64)
+    elif case.dtype == BF16:
+        qf = (case.q[b].astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+        kf = (case.k[b, members[0]].astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    else:
+        tq = torch.from_numpy(np.ascontiguousarray(case.q[b])).view(torch.float8_e4m3fn)
+        tk = torch.from_numpy(np.ascontiguousarray(case.k[b, members[0]])).view(torch.float8_e4m3fn)
+        qf = tq.to(torch.float64).numpy() * case.q_scale
+        kf = tk.to(torch.float64).numpy() * scale
+    row = np.empty((case.Hkv, case.D), np.float32)
+    for g in range(case.Hkv):
+        qsum = qf[case.V_full:, g * G:(g + 1) * G, :].sum(axis=(0, 1))
+        u = qsum / max(np.linalg.norm(qsum), 1e-30)
+        row[g] = (kf[g] + beta * np.sqrt(case.D) * u).astype(np.float32)
+    bits = encode_with_scale(row, case.dtype, scale) if case.dtype == FP8 else encode(row, case.dtype)[0]
+    for j in members:
+        k[b, j] = bits
+    return dataclasses.replace(case, k=k)
+

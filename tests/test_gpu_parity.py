@@ -5,6 +5,7 @@ oracle only. Selection follows the near-tie band rule; index lists, lengths
 and gathered rows are bit-exact; attention is held to the per-precision
 tolerances in parity_util.
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -14,7 +15,7 @@ import torch
 import oracle
 import paper_2506_07416_amd as lv
 import synth
-from parity_util import (bits_of, check_attention, check_selection, log, sample_rows,
+from parity_util import (bits_of, check_attention, check_selection, check_view_keep, log,
                          score_rel_err, to_device, to_float64)
 
 pytestmark = pytest.mark.gpu
@@ -46,8 +47,13 @@ def run_select(case, keep_ratio=None, gather=True, query_rows=None):
     return res
 
 
-def check_select(case, g, ref, label):
-    """Selection-stage parity; returns True when every sample's kept set equals the oracle's."""
+def check_select(case, g, ref, label, exact=False):
+    """Selection-stage parity; returns True when every sample's kept set equals
+    the oracle's. exact: the kept indices must equal the oracle's bit for bit
+    (cases whose exact ties the lower-position rule decides)."""
+    vs = oracle.view_scores(case.view_logit, case.view_lexical, case.w_lexical)
+    check_view_keep(vs, case.threshold, g["view_keep"])
+    # the workloads' view logits lie far from the threshold: the masks are the oracle's
     assert np.array_equal(g["view_keep"], ref["view_keep"]), label
     assert np.array_equal(g["token_keep"], ref["token_keep"]), label
     assert np.array_equal(g["n_vis"], ref["V_b"]), label
@@ -67,6 +73,9 @@ def check_select(case, g, ref, label):
         got = bits_of(g["dev"][name][:g["cu"][-1]])
         want = np.concatenate([src[b, g["kept_index"][g["cu"][b]:g["cu"][b + 1]]] for b in range(case.B)])
         assert np.array_equal(got.reshape(want.shape).view(want.dtype), want), f"{label}: {name} bits"
+    if exact:
+        assert np.array_equal(g["kept_index"], ref["kept_index"]), f"{label}: kept_index differs"
+        identical = True
     log(f"{label}: score rel err {err:.2e}, band sizes {bands}, identical sets {identical}")
     return identical
 
@@ -86,6 +95,8 @@ def test_patch_select_matches_oracle(cfg):
     case = synth.config_case(cfg, Tv=8, T=4, Hq=4, Hkv=2 if cfg > 2 else 4, D=64, dtype="f32")
     log(f"patch_select cfg{cfg}: B={case.B} N={case.N}")
     g = run_select(case, gather=False)
+    vs = oracle.view_scores(case.view_logit, None, case.w_lexical)
+    check_view_keep(vs, case.threshold, g["view_keep"])
     view_keep = oracle.patch_select(case.view_logit, None, case.w_lexical, case.threshold)
     assert np.array_equal(g["view_keep"], view_keep)
     assert np.array_equal(g["token_keep"], oracle.token_keep_from_views(view_keep, case.view_offsets, case.S))
@@ -102,10 +113,37 @@ def test_patch_select_random_logits_lexical_fallback():
         vk, tk, nv = lv.patch_select(torch.from_numpy(logit).cuda(), off, S, w, tau,
                                      view_lexical=torch.from_numpy(lex).cuda())
         torch.cuda.synchronize()
-        ref = oracle.patch_select(logit, lex, w, tau)
-        assert np.array_equal(vk.cpu().numpy(), ref), (w, tau)
-        assert np.array_equal(tk.cpu().numpy(), oracle.token_keep_from_views(ref, off, S))
-        assert np.array_equal(nv.cpu().numpy(), oracle.token_keep_from_views(ref, off, S)[:, :50].sum(1))
+        got = vk.cpu().numpy()
+        check_view_keep(oracle.view_scores(logit, lex, w), tau, got)
+        # the token mask and counts follow the GPU's own view mask exactly
+        assert np.array_equal(tk.cpu().numpy(), oracle.token_keep_from_views(got, off, S))
+        assert np.array_equal(nv.cpu().numpy(), oracle.token_keep_from_views(got, off, S)[:, :50].sum(1))
+        assert np.array_equal(got, oracle.patch_select(logit, lex, w, tau)), (w, tau)
+
+
+def test_patch_select_near_threshold():
+    """Fused scores within a few ulps of the threshold: views in the 1e-6 band
+    may fall either way, every other view and the fallback are exact."""
+    rng = np.random.default_rng(12)
+    B, N, S = 64, 6, 70
+    off = np.array([0, 10, 20, 30, 40, 50, 60], np.int32)
+    tau = 0.62
+    x0 = math.log(tau / (1 - tau))                 # sigmoid(x0) = tau
+    logit = (x0 + rng.integers(-4, 5, (B, N)) * 2e-7 * rng.random((B, N))).astype(np.float32)
+    logit[::7] -= 3.0                              # rows where nothing passes: the fallback
+    lex = rng.random((B, N)).astype(np.float32)
+    total_band = 0
+    for w in (0.0, 1e-3):
+        vk, tk, nv = lv.patch_select(torch.from_numpy(logit).cuda(), off, S, w, tau,
+                                     view_lexical=torch.from_numpy(lex).cuda())
+        torch.cuda.synchronize()
+        got = vk.cpu().numpy()
+        n_band = check_view_keep(oracle.view_scores(logit, lex, w), tau, got)
+        assert np.array_equal(tk.cpu().numpy(), oracle.token_keep_from_views(got, off, S))
+        assert np.array_equal(nv.cpu().numpy(), oracle.token_keep_from_views(got, off, S)[:, :60].sum(1))
+        log(f"near-threshold w={w}: {n_band} of {B * N} views inside the band")
+        total_band += n_band
+    assert total_band > 0
 
 
 # ----------------------------------------------------------------------------- attention
@@ -307,63 +345,172 @@ def test_full_keep_equals_unpruned_attention():
     assert torch.equal(o_chain[:case.S].view(torch.int16), o_full.view(torch.int16))
 
 
+# ----------------------------------------------------------------------------- exact ties
+
+def kept_visual_scores(g, b, V_full):
+    return g["scores"][b, :V_full][g["token_keep"][b, :V_full] == 1]
+
+
+@pytest.mark.parametrize("which", ["cfg2", "cfg3-r0.5"])
+def test_exact_ties_zero_queries(which):
+    """All queries zero: every attention row is uniform over its visible keys,
+    so every kept visual token scores (1/T)*sum_t 1/(V_b+t+1) exactly and all
+    of them tie. The GPU scores must be bitwise equal and the kept set must be
+    the lowest k_b positions, index for index; the attention over the chain is
+    then a prefix mean of V."""
+    base = synth.config_case(2) if which == "cfg2" else synth.config_case(3, keep_ratio=0.5)
+    case = synth.with_zero_queries(base)
+    log(f"zero-query ties {which}: S={case.S} Hq={case.Hq} Hkv={case.Hkv} r={case.keep_ratio}")
+    g = run_select(case)
+    ref = oracle.run_path(case, attention=False)
+    T = case.S - case.V_full
+    for b in range(case.B):
+        vals = kept_visual_scores(g, b, case.V_full)
+        assert np.unique(vals).size == 1, f"sample {b}: {np.unique(vals).size} distinct GPU scores"
+        V_b = int(ref["V_b"][b])
+        closed = sum(1.0 / (V_b + t + 1) for t in range(T)) / T
+        assert abs(vals[0] - closed) <= 1e-6 * closed, (vals[0], closed)
+        kept = np.nonzero(ref["token_keep"][b, :case.V_full])[0]
+        assert np.array_equal(ref["selected"][b], kept[:int(ref["k_b"][b])])   # the oracle's tie rule
+    check_select(case, g, ref, f"zero-query {which}", exact=True)
+    cu = g["cu"]
+    o = attention_on(case, g["dev"]["qc"], g["dev"]["kc"], g["dev"]["vc"], g["dev"]["cu_seqlens"],
+                     int(np.max(np.diff(cu))))
+    ref_o = oracle.run_path(case)["o"]
+    stats = check_attention(to_float64(o[:cu[-1]]), ref_o, "bf16", which)
+    log(f"  attention (prefix means) {stats}")
+
+
+@pytest.mark.parametrize("which", ["cfg2", "bf16-gqa", "fp8-gqa"])
+def test_exact_ties_duplicated_keys_straddle_k(which):
+    """Six kept visual tokens share one key row (bitwise), lifted above the
+    other tokens; k is chosen so that the group straddles rank k. The members'
+    GPU scores must be bitwise equal and exactly the lower-positioned members
+    must be kept."""
+    if which == "cfg2":
+        base = synth.config_case(2)
+    elif which == "bf16-gqa":
+        base = synth.config_case(4, B=1, Tv=200, T=24, n_masked=1)
+    else:
+        base = synth.config_case(5, B=1, Tv=256, T=32)
+    vk = oracle.patch_select(base.view_logit, None, base.w_lexical, base.threshold)
+    tk = oracle.token_keep_from_views(vk, base.view_offsets, base.S)
+    cand = np.nonzero(tk[0, :base.V_full])[0]
+    n = len(cand)
+    members = sorted({int(cand[i]) for i in (n // 3, 7, n // 6, n // 2, (2 * n) // 3, n - 3)})
+    case = synth.with_duplicated_keys(base, 0, members, beta=3.0)
+    q64, k64, _ = oracle.decode_inputs(case)
+    s = oracle.token_scores(q64, k64, tk, case.V_full, case.Hq, case.Hkv, 1 / math.sqrt(case.D))[0]
+    sg = s[members[0]]
+    assert np.all(s[members] == sg), "oracle: identical keys must score identically"
+    others = np.setdiff1d(cand, members)
+    assert np.min(np.abs(s[others] - sg)) > 1e-5 * sg, "group not isolated from the other scores"
+    above = int(np.sum(s[others] > sg))
+    k = above + len(members) // 2
+    r = k / n
+    assert oracle.keep_count(r, n) == k
+    want = np.sort(np.concatenate([others[s[others] > sg], members[:len(members) // 2]]))
+    log(f"duplicated keys {which}: V_b={n} members {members} above {above} k={k}")
+    g = run_select(case, keep_ratio=r)
+    ref = oracle.run_path(case, keep_ratio=r, attention=False)
+    assert np.array_equal(ref["selected"][0], want)                       # the oracle's tie rule
+    got_s = g["scores"][0, members]
+    assert np.unique(got_s).size == 1, f"GPU member scores differ: {got_s}"
+    case_r = dataclasses.replace(case, keep_ratio=r)
+    check_select(case_r, g, ref, f"duplicated keys {which}", exact=True)
+    assert np.array_equal(g["kept_index"][:k], want)
+
+
 # ----------------------------------------------------------------------------- full sizes
+
+def full_size_chain(case, label, kind, keep_ratio=None):
+    """The whole chain at a full workload size: selection against the oracle,
+    then attention over every packed row and head. When the kept sets equal
+    the oracle's, the attention runs on the chain's own compacted buffers;
+    otherwise (near-ties) on the oracle's compacted inputs. The attention grid
+    is sized from the host bound floor(r*V_full + 1e-6) + T, as the benchmark
+    sizes it."""
+    r = case.keep_ratio if keep_ratio is None else keep_ratio
+    g = run_select(case, keep_ratio=r)
+    ref = oracle.run_path(case, keep_ratio=r, attention=False)
+    identical = check_select(case, g, ref, label)
+    T = case.S - case.V_full
+    bound = oracle.keep_count(r, case.V_full) + T
+    cu = ref["cu_seqlens"]
+    assert int(np.max(np.diff(cu))) <= bound
+    if identical:
+        o = attention_on(case, g["dev"]["qc"], g["dev"]["kc"], g["dev"]["vc"], g["dev"]["cu_seqlens"], bound)
+    else:
+        qc, kc, vc = (to_device(ref[n], case.dtype) for n in ("qc_bits", "kc_bits", "vc_bits"))
+        o = attention_on(case, qc, kc, vc, cu, bound)
+    q64, k64, v64 = oracle.decode_inputs(case)
+    ref_o = oracle.prefill_attention(oracle.gather_rows(q64, ref["kept_index"], cu),
+                                     oracle.gather_rows(k64, ref["kept_index"], cu),
+                                     oracle.gather_rows(v64, ref["kept_index"], cu),
+                                     cu, case.Hq, case.Hkv, 1 / math.sqrt(case.D))
+    stats = check_attention(to_float64(o[:cu[-1]]), ref_o, kind, label)
+    log(f"  {label}: identical sets {identical}; attention over all {cu[-1]} rows x {case.Hq} heads {stats}")
+
 
 @pytest.mark.parametrize("r", synth.CFG3_KEEP_SWEEP)
 def test_cfg3_full_size(r):
     case = synth.config_case(3, keep_ratio=r)
     log(f"cfg3 full size r={r}: S={case.S} Hq={case.Hq} Hkv={case.Hkv}")
-    g = run_select(case)
-    ref = oracle.run_path(case, attention=False)
-    identical = check_select(case, g, ref, f"cfg3 r={r}")
-    max_len = int(np.max(np.diff(ref["cu_seqlens"])))
-    qc = to_device(ref["qc_bits"], case.dtype)
-    kc = to_device(ref["kc_bits"], case.dtype)
-    vc = to_device(ref["vc_bits"], case.dtype)
-    o = attention_on(case, qc, kc, vc, ref["cu_seqlens"], max_len)
-    rows = sample_rows(ref["cu_seqlens"], 24, seed=7)
-    q64, k64, v64 = oracle.decode_inputs(case)
-    ref_o = oracle.prefill_attention(oracle.gather_rows(q64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(k64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(v64, ref["kept_index"], ref["cu_seqlens"]),
-                                     ref["cu_seqlens"], case.Hq, case.Hkv, 1 / math.sqrt(case.D), rows=rows)
-    stats = check_attention(to_float64(o)[rows], ref_o[rows], "bf16", f"cfg3 r={r}")
-    log(f"  identical sets {identical}; attention on {len(rows)} sampled rows {stats}")
+    full_size_chain(case, f"cfg3 r={r}", "bf16")
+
+
+def test_cfg3_full_size_peaked():
+    # Q, K ~ N(0,1): logits of standard deviation ~1 instead of ~1/D
+    case = synth.config_case(3, run=1, keep_ratio=0.5, peaked=True)
+    log("cfg3 full size peaked r=0.5")
+    full_size_chain(case, "cfg3 peaked r=0.5", "bf16")
 
 
 def test_cfg4_full_size_ragged():
     case = synth.config_case(4)
     log(f"cfg4 full size: B={case.B} masked={[len(m) for m in case.masked_views]}")
-    g = run_select(case)
-    ref = oracle.run_path(case, attention=False)
-    check_select(case, g, ref, "cfg4")
-    max_len = int(np.max(np.diff(ref["cu_seqlens"])))
-    qc, kc, vc = (to_device(ref[n], case.dtype) for n in ("qc_bits", "kc_bits", "vc_bits"))
-    o = attention_on(case, qc, kc, vc, ref["cu_seqlens"], max_len)
-    rows = sample_rows(ref["cu_seqlens"], 8, seed=8)
-    q64, k64, v64 = oracle.decode_inputs(case)
-    ref_o = oracle.prefill_attention(oracle.gather_rows(q64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(k64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(v64, ref["kept_index"], ref["cu_seqlens"]),
-                                     ref["cu_seqlens"], case.Hq, case.Hkv, 1 / math.sqrt(case.D), rows=rows)
-    stats = check_attention(to_float64(o)[rows], ref_o[rows], "bf16", "cfg4")
-    log(f"  attention on {len(rows)} sampled rows {stats}")
+    full_size_chain(case, "cfg4", "bf16")
 
 
 def test_cfg5_full_size_fp8():
     case = synth.config_case(5)
     log(f"cfg5 full size: B={case.B} fp8 e4m3, scales {case.q_scale:.3g} {case.k_scale:.3g} {case.v_scale:.3g}")
-    g = run_select(case)
-    ref = oracle.run_path(case, attention=False)
-    check_select(case, g, ref, "cfg5")
-    max_len = int(np.max(np.diff(ref["cu_seqlens"])))
-    qc, kc, vc = (to_device(ref[n], case.dtype) for n in ("qc_bits", "kc_bits", "vc_bits"))
-    o = attention_on(case, qc, kc, vc, ref["cu_seqlens"], max_len)
-    rows = sample_rows(ref["cu_seqlens"], 8, seed=9)
-    q64, k64, v64 = oracle.decode_inputs(case)
-    ref_o = oracle.prefill_attention(oracle.gather_rows(q64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(k64, ref["kept_index"], ref["cu_seqlens"]),
-                                     oracle.gather_rows(v64, ref["kept_index"], ref["cu_seqlens"]),
-                                     ref["cu_seqlens"], case.Hq, case.Hkv, 1 / math.sqrt(case.D), rows=rows)
-    stats = check_attention(to_float64(o)[rows], ref_o[rows], "fp8", "cfg5")
-    log(f"  attention on {len(rows)} sampled rows {stats}")
+    full_size_chain(case, "cfg5", "fp8")
+
+
+def test_cfg5_full_size_fp8_peaked():
+    case = synth.config_case(5, run=1, peaked=True)
+    log(f"cfg5 full size peaked: B={case.B} masked={[len(m) for m in case.masked_views]}")
+    full_size_chain(case, "cfg5 peaked", "fp8")
+
+
+@pytest.mark.parametrize("r", synth.CFG3_KEEP_SWEEP)
+def test_fp8_batch1_keep_sweep(r):
+    """The 6x1024 batch-1 shape in E4M3 across the keep-ratio sweep."""
+    case = synth.config_case(3, dtype="fp8", keep_ratio=r)
+    log(f"fp8 6x1024 batch 1 r={r}: scales {case.q_scale:.3g} {case.k_scale:.3g} {case.v_scale:.3g}")
+    full_size_chain(case, f"fp8 batch1 r={r}", "fp8")
+
+
+# ----------------------------------------------------------------------------- grid bound
+
+@pytest.mark.parametrize("dtype", ["bf16", "fp8", "f32"])
+def test_attention_grid_bound_above_lengths(dtype):
+    """max_seqlen only sizes the grid: a bound far above the real lengths (the
+    uncompressed S) gives bitwise the output of the tight bound, and both match
+    the oracle."""
+    lens = [700, 130, 0, 1, 257] if dtype != "f32" else [150, 0, 65, 1]
+    Hq, Hkv, D = (32, 8, 128) if dtype != "f32" else (4, 2, 64)
+    qb, kb, vb, scales, cu = synth.random_attention_inputs(lens, Hq, Hkv, D, dtype, seed=321, peaked=True)
+    q, k, v = (to_device(x, dtype) for x in (qb, kb, vb))
+    cu_d = torch.from_numpy(cu).cuda()
+    outs = []
+    for bound in (max(lens), 6272):
+        o = lv.prefill_attn(q, k, v, cu_d, bound, q_scale=scales[0], k_scale=scales[1], v_scale=scales[2])
+        torch.cuda.synchronize()
+        outs.append(o)
+    assert torch.equal(outs[0].view(torch.uint8), outs[1].view(torch.uint8))
+    q64, k64, v64 = (oracle.litevlm.decode_stored(x, dtype, sc) for x, sc in zip((qb, kb, vb), scales))
+    ref = oracle.prefill_attention(q64, k64, v64, cu, Hq, Hkv, 1 / math.sqrt(D))
+    stats = check_attention(to_float64(outs[1]), ref, attn_kind(dtype), f"bound {dtype}")
+    log(f"  grid bound 6272 vs {max(lens)}: bitwise equal; {stats}")

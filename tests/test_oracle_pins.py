@@ -193,6 +193,22 @@ def test_patch_select_closed_forms():
     assert keep.tolist() == [[0, 1, 0, 0]]
 
 
+def test_view_scores_match_expit_in_float64():
+    from scipy.special import expit
+    rng = np.random.default_rng(5)
+    logit = rng.normal(0, 3, (7, 6))
+    lex = rng.random((7, 6))
+    for w in (0.0, 0.25, 1.0):
+        s = oracle.view_scores(logit, lex, w)
+        assert s.dtype == np.float64
+        assert np.allclose(s, w * lex + (1 - w) * expit(logit), rtol=1e-15, atol=0)
+    assert np.allclose(oracle.view_scores(logit, None, 0.3), 0.7 * expit(logit), rtol=1e-15, atol=0)
+    # the decision is taken in float64: a score 1e-9 above the threshold is kept
+    # (in float32, sigmoid(4e-9) rounds to exactly 0.5 and the view would drop)
+    keep = oracle.patch_select(np.array([[4e-9, -4e-9, 0.0]]), None, 0.0, 0.5)
+    assert keep.tolist() == [[1, 0, 0]]
+
+
 def test_patch_select_brute_force_all_masks():
     # for every subset of 6 views, logits +-8 select exactly that subset (or the
     # fallback to view 0 for the empty subset, all scores tie there)
