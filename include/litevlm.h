@@ -33,7 +33,9 @@
  *     the caller's next synchronisation, as usual in HIP.
  *   - Results are deterministic: identical inputs give bitwise-identical outputs
  *     (fixed reduction orders, no floating-point atomics).
- *   - Calls are reentrant and keep no global mutable state.
+ *   - Calls are reentrant and keep no global mutable state, except
+ *     litevlm_token_score_topk_noalloc, which works in a device array of the
+ *     library (see there).
  *
  * Sequence layout: visual tokens of view v occupy positions
  * [view_offsets[v], view_offsets[v+1]), views in order, view_offsets[0] = 0,
@@ -165,6 +167,36 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
                                           double keep_ratio, float* scores, int32_t* kept_index,
                                           int32_t* cu_seqlens, void* qc, void* kc, void* vc,
                                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Size of the device scratch array of litevlm_token_score_topk_noalloc (8 MiB
+ * per GPU, held from the first such call on a GPU until the process ends). */
+#define LITEVLM_NOALLOC_SCRATCH_BYTES (8u << 20)
+
+/*
+ * litevlm_token_score_topk_noalloc - litevlm_token_score_topk for callers that
+ * cannot allocate device memory (code under HIP graph capture, serving loops
+ * that forbid allocation): the same computation, arguments, layouts and
+ * results, with the workspace taken from a static device array of the library
+ * instead of a caller buffer. It calls no hipMalloc, hipFree or allocating
+ * routine; the array's device address is looked up once per device (on the
+ * first call made with that device current).
+ *
+ * Limit: the workspace of the sizes, litevlm_token_score_topk_workspace(B, S,
+ * V_full, Hq, Hkv, D), must fit LITEVLM_NOALLOC_SCRATCH_BYTES, else the call
+ * returns LITEVLM_ERR_WORKSPACE and launches nothing. Every call on one GPU
+ * shares that GPU's array, so calls that may overlap on one GPU (other
+ * streams, other host threads) race and give undefined results; calls on one
+ * stream are ordered and safe. The array keeps the last call's contents, which
+ * no call reads before writing.
+ */
+litevlm_status_t litevlm_token_score_topk_noalloc(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                                  int32_t Hq, int32_t Hkv, int32_t D,
+                                                  const void* q, const void* k, const void* v,
+                                                  float softmax_scale, float q_scale, float k_scale,
+                                                  float v_scale, const uint8_t* token_keep,
+                                                  double keep_ratio, float* scores, int32_t* kept_index,
+                                                  int32_t* cu_seqlens, void* qc, void* kc, void* vc,
+                                                  void* stream);
 
 /* Bytes of device workspace litevlm_token_score_topk_rows needs for these
  * sizes (0 when the sizes or query_rows are invalid). */

@@ -84,14 +84,16 @@ def token_score_topk(q: torch.Tensor, k: torch.Tensor, v: Optional[torch.Tensor]
                      softmax_scale: Optional[float] = None, q_scale: float = 1.0,
                      k_scale: float = 1.0, v_scale: float = 1.0, gather: bool = True,
                      workspace: Optional[torch.Tensor] = None, out: Optional[dict] = None,
-                     query_rows: Optional[int] = None) -> dict:
+                     query_rows: Optional[int] = None, noalloc: bool = False) -> dict:
     """Scores, top-k and compaction. q: [B,S,Hq,D], k/v: [B,S,Hkv,D] (fp32, bf16 or
     E4M3 bytes). Returns a dict of device tensors: scores [B,V_full] fp32,
     kept_index [B*S] int32 (packed, valid up to cu_seqlens[B]), cu_seqlens [B+1],
     and when gather is set qc [B*S,Hq,D], kc/vc [B*S,Hkv,D] (valid rows likewise).
     ``out`` may supply preallocated tensors under the same keys (plus "workspace").
     query_rows = n scores with the last n text tokens as the only query rows
-    (litevlm_token_score_topk_rows); None uses every text token."""
+    (litevlm_token_score_topk_rows); None uses every text token. noalloc calls
+    litevlm_token_score_topk_noalloc, whose workspace is the library's own
+    device array (no workspace tensor is made or passed)."""
     lib = load()
     B, S, Hq, D = q.shape
     Hkv = k.shape[2]
@@ -106,6 +108,16 @@ def token_score_topk(q: torch.Tensor, k: torch.Tensor, v: Optional[torch.Tensor]
         o.setdefault("qc", torch.empty((B * S, Hq, D), dtype=q.dtype, device=dev))
         o.setdefault("kc", torch.empty((B * S, Hkv, D), dtype=k.dtype, device=dev))
         o.setdefault("vc", torch.empty((B * S, Hkv, D), dtype=v.dtype, device=dev))
+    if noalloc:
+        if query_rows is not None or workspace is not None:
+            raise ValueError("the no-alloc call scores every text row and takes no workspace")
+        st = lib.litevlm_token_score_topk_noalloc(
+            dtype_code(q.dtype), B, S, V_full, Hq, Hkv, D, _ptr(q), _ptr(k), _ptr(v), float(softmax_scale),
+            float(q_scale), float(k_scale), float(v_scale), _ptr(token_keep), float(keep_ratio),
+            _ptr(o["scores"]), _ptr(o["kept_index"]), _ptr(o["cu_seqlens"]), _ptr(o.get("qc")),
+            _ptr(o.get("kc")), _ptr(o.get("vc")), _stream(dev))
+        _abi.check(st, "litevlm_token_score_topk_noalloc")
+        return o
     nbytes = workspace_bytes(B, S, V_full, Hq, Hkv, D, query_rows)
     ws = workspace if workspace is not None else o.get("workspace")
     if ws is None:

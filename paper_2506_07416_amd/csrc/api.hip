@@ -3,6 +3,8 @@
 // HIP call, so an error status means nothing was enqueued or written.
 #include <math.h>
 
+#include <mutex>
+
 #include "launch.hpp"
 
 using namespace litevlm;
@@ -101,14 +103,17 @@ size_t litevlm_token_score_topk_workspace(int32_t B, int32_t S, int32_t V_full, 
   return litevlm_token_score_topk_rows_workspace(B, S, V_full, Hq, Hkv, D, S - V_full);
 }
 
-litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
-                                               int32_t Hq, int32_t Hkv, int32_t D, int32_t query_rows,
-                                               const void* q, const void* k, const void* v,
-                                               float softmax_scale, float q_scale, float k_scale,
-                                               float v_scale, const uint8_t* token_keep, double keep_ratio,
-                                               float* scores, int32_t* kept_index, int32_t* cu_seqlens,
-                                               void* qc, void* kc, void* vc, void* workspace,
-                                               size_t workspace_bytes, void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Validation of every argument of the scoring call except the workspace.
+litevlm_status_t check_score_args(int32_t dtype, int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                  int32_t Hkv, int32_t D, int32_t query_rows, const void* q, const void* k,
+                                  const void* v, float softmax_scale, float q_scale, float k_scale,
+                                  float v_scale, double keep_ratio, const float* scores,
+                                  const int32_t* kept_index, const int32_t* cu_seqlens, const void* qc,
+                                  const void* kc, const void* vc) {
   if (!q || !k || !scores || !kept_index || !cu_seqlens) return LITEVLM_ERR_NULL_POINTER;
   if (vc && !v) return LITEVLM_ERR_NULL_POINTER;
   if (!valid_dtype(dtype)) return LITEVLM_ERR_UNSUPPORTED;
@@ -121,14 +126,19 @@ litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t
   if (dtype != LITEVLM_FP8_E4M3 && (q_scale != 1.f || k_scale != 1.f || v_scale != 1.f))
     return LITEVLM_ERR_BAD_VALUE;
   if (!(keep_ratio >= 0.0 && keep_ratio <= 1.0)) return LITEVLM_ERR_BAD_VALUE;
-  const void* big[] = {q, k, v, qc, kc, vc, workspace};
+  const void* big[] = {q, k, v, qc, kc, vc};
   for (const void* p : big)
     if (p && !aligned(p, 16)) return LITEVLM_ERR_MISALIGNED;
   if (!aligned(scores, 4) || !aligned(kept_index, 4) || !aligned(cu_seqlens, 4))
     return LITEVLM_ERR_MISALIGNED;
-  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv, query_rows).total;
-  if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
+  return LITEVLM_OK;
+}
 
+litevlm_status_t launch_score(int32_t dtype, int32_t B, int32_t S, int32_t V_full, int32_t Hq, int32_t Hkv,
+                              int32_t D, int32_t query_rows, const void* q, const void* k, const void* v,
+                              float softmax_scale, float q_scale, float k_scale, const uint8_t* token_keep,
+                              double keep_ratio, float* scores, int32_t* kept_index, int32_t* cu_seqlens,
+                              void* qc, void* kc, void* vc, void* workspace, void* stream) {
   ScoreArgs a;
   a.dtype = dtype;
   a.B = B;
@@ -152,6 +162,80 @@ litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t
   a.vc = vc;
   a.workspace = workspace;
   return hip_status(launch_token_score_topk(a, static_cast<hipStream_t>(stream)));
+}
+
+// Device scratch of litevlm_token_score_topk_noalloc: the workspace of the
+// scoring call (per-split row statistics, fixed-point column sums) for callers
+// that cannot allocate. Each GPU holds its own copy for the life of the
+// process. In host code the name is only a host-side stand-in: its device
+// address comes from hipGetSymbolAddress, once per device, and only that
+// address is ever passed to kernels.
+static __device__ __align__(256) uint8_t scratch[LITEVLM_NOALLOC_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};  // device address of `scratch` per device ordinal
+
+// The scratch array's device address on the current device, looked up on the
+// first call made with that device current.
+litevlm_status_t device_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) return LITEVLM_ERR_HIP;
+  if (dev < 0 || dev >= kMaxDevices) return LITEVLM_ERR_UNSUPPORTED;
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || p == nullptr) return LITEVLM_ERR_HIP;
+    g_scratch_ptr[dev] = p;
+  }
+  *out = g_scratch_ptr[dev];
+  return LITEVLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+litevlm_status_t litevlm_token_score_topk_noalloc(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                                  int32_t Hq, int32_t Hkv, int32_t D, const void* q,
+                                                  const void* k, const void* v, float softmax_scale,
+                                                  float q_scale, float k_scale, float v_scale,
+                                                  const uint8_t* token_keep, double keep_ratio, float* scores,
+                                                  int32_t* kept_index, int32_t* cu_seqlens, void* qc, void* kc,
+                                                  void* vc, void* stream) {
+  const int32_t T = S > V_full ? S - V_full : 1;
+  const litevlm_status_t st =
+      check_score_args(dtype, B, S, V_full, Hq, Hkv, D, T, q, k, v, softmax_scale, q_scale, k_scale, v_scale,
+                       keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc);
+  if (st != LITEVLM_OK) return st;
+  if (score_workspace_layout(B, S, V_full, Hq, Hkv, T).total > LITEVLM_NOALLOC_SCRATCH_BYTES)
+    return LITEVLM_ERR_WORKSPACE;
+  void* ws = nullptr;
+  const litevlm_status_t sc = device_scratch(&ws);
+  if (sc != LITEVLM_OK) return sc;
+  // the kernels need the scratch contents on entry to be nothing in particular
+  // (sweep 1 clears the column sums itself), so no clearing is enqueued here
+  return launch_score(dtype, B, S, V_full, Hq, Hkv, D, T, q, k, v, softmax_scale, q_scale, k_scale, token_keep,
+                      keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc, ws, stream);
+}
+
+litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
+                                               int32_t Hq, int32_t Hkv, int32_t D, int32_t query_rows,
+                                               const void* q, const void* k, const void* v,
+                                               float softmax_scale, float q_scale, float k_scale,
+                                               float v_scale, const uint8_t* token_keep, double keep_ratio,
+                                               float* scores, int32_t* kept_index, int32_t* cu_seqlens,
+                                               void* qc, void* kc, void* vc, void* workspace,
+                                               size_t workspace_bytes, void* stream) {
+  const litevlm_status_t st =
+      check_score_args(dtype, B, S, V_full, Hq, Hkv, D, query_rows, q, k, v, softmax_scale, q_scale, k_scale,
+                       v_scale, keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc);
+  if (st != LITEVLM_OK) return st;
+  if (workspace && !aligned(workspace, 16)) return LITEVLM_ERR_MISALIGNED;
+  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv, query_rows).total;
+  if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
+  return launch_score(dtype, B, S, V_full, Hq, Hkv, D, query_rows, q, k, v, softmax_scale, q_scale, k_scale,
+                      token_keep, keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc, workspace, stream);
 }
 
 litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,
