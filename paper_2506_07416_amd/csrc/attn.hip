@@ -28,7 +28,7 @@ struct AttnParams {
   const void* v;
   const int32_t* cu;
   void* o;
-  int B, Hq, Hkv, G;
+  int B, Hq, Hkv, G, n_mtiles, n_work, per_xcd;
   float scale_log2, out_scale;
 };
 
@@ -74,93 +74,23 @@ __device__ __forceinline__ int tile_key(int nb, int rho) {
   return 32 * nb + swap23(rho);
 }
 
-// Work item of a flat grid. Items are (KV head, query tile from the last one
-// down, sample, head in group), restricted to the live tiles (tile mt of
-// sample b is live when mt*BM < len_b), numbered in that order and dealt to the
-// 8 XCDs in contiguous ranges: an XCD owns whole KV heads across the batch, so
-// workgroups sharing K/V sit behind the same L2, ragged samples spread evenly
-// over the XCDs, and within an XCD the longest causal tiles start first. The
-// grid is sized from the host bound on the lengths; workgroup L (on XCD L % 8)
-// takes the (L / 8)-th item of its XCD's range, so the surplus workgroups come
-// after every live one in dispatch order and exit at once.
-//
-// Every wave decodes the item itself from cu_seqlens (lane i holds samples
-// i, i+64, ...; B <= 256), so no barrier or LDS is involved. On return seq0
-// and len describe sample b.
-struct WorkItem {
-  int b, h, mt, seq0, len;
-};
-
-template <int BM>
-__device__ __forceinline__ bool decode_work(const AttnParams& p, WorkItem& it) {
-  constexpr int NC = (LITEVLM_MAX_BATCH + 63) / 64;
-  const int lane = threadIdx.x & 63;
-  const int nch = (p.B + 63) >> 6;
-  int lo[NC], nt[NC];
-  int sum = 0, mx = 0;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const int bb = 64 * c + lane;
-    lo[c] = 0;
-    nt[c] = 0;
-    if (c < nch && bb < p.B) {
-      lo[c] = p.cu[bb];
-      nt[c] = (p.cu[bb + 1] - lo[c] + BM - 1) / BM;
-    }
-    sum += nt[c];
-    mx = max(mx, nt[c]);
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    sum += __shfl_xor(sum, off, kWave);
-    mx = max(mx, __shfl_xor(mx, off, kWave));
-  }
-  const int per_g = sum * p.G;
-  const int n_live = per_g * p.Hkv;
-  const int per_xcd = (n_live + 7) >> 3;
-  const int L = blockIdx.x, j = L >> 3;
-  if (j >= per_xcd) return false;
-  const int w = (L & 7) * per_xcd + j;
-  if (w >= n_live) return false;
-  const int g = w / per_g;
-  int r = w - g * per_g;
-  // query tile: walk down from the longest sample's last tile, G*(live
-  // samples) items per tile (r < per_g, so the walk ends at tile 0 at the latest)
-  int mt = mx - 1;
-  for (; mt > 0; --mt) {
-    int cnt = 0;
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-      if (c < nch) cnt += __popcll(__ballot(nt[c] > mt));
-    if (r < cnt * p.G) break;
-    r -= cnt * p.G;
-  }
-  int idx = r / p.G;
-  const int hh = r - idx * p.G;
-  // the idx-th live sample of this tile, in ascending order
-  it.b = -1;
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    if (c >= nch) break;
-    const uint64_t m = __ballot(nt[c] > mt);
-    const int pc = __popcll(m);
-    if (idx < pc) {
-      const int rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0));
-      const uint64_t hit = __ballot(((m >> lane) & 1ull) && rank == idx);
-      const int src = __builtin_ctzll(hit);
-      it.b = 64 * c + src;
-      it.seq0 = __shfl(lo[c], src, kWave);
-      break;
-    }
-    idx -= pc;
-  }
-  if (it.b < 0) return false;  // not reached for non-decreasing cu_seqlens
-  // wave-uniform results, kept in scalar registers
-  it.b = __builtin_amdgcn_readfirstlane(it.b);
-  it.seq0 = __builtin_amdgcn_readfirstlane(it.seq0);
-  it.len = p.cu[it.b + 1] - it.seq0;
-  it.h = __builtin_amdgcn_readfirstlane(g * p.G + hh);
-  it.mt = __builtin_amdgcn_readfirstlane(mt);
+// Work item of a flat grid. Items are ordered (KV head, query tile heaviest
+// first, sample, head in group) and dealt to the 8 XCDs in contiguous ranges:
+// an XCD owns whole KV heads across the batch, so workgroups sharing K/V sit
+// behind the same L2 while ragged samples spread evenly over the XCDs, and
+// within an XCD the longest causal tiles start first.
+__device__ __forceinline__ bool decode_work(const AttnParams& p, int& b, int& h, int& mt) {
+  const int L = blockIdx.x;
+  const int w = (L & 7) * p.per_xcd + (L >> 3);
+  if (w >= p.n_work) return false;
+  const int hh = w % p.G;
+  int rest = w / p.G;
+  b = rest % p.B;
+  rest /= p.B;
+  const int mrev = rest % p.n_mtiles;
+  const int g = rest / p.n_mtiles;
+  h = g * p.G + hh;
+  mt = p.n_mtiles - 1 - mrev;
   return true;
 }
 
@@ -206,10 +136,11 @@ attn_bf16_kernel(AttnParams p) {
   // explicit wait + barrier below orders each buffer's copy before its reads.
   __shared__ __attribute__((aligned(1024))) uint8_t kvl[4 * TB];
 
-  WorkItem it;
-  if (!decode_work<BM>(p, it)) return;
-  const int h = it.h, seq0 = it.seq0, len = it.len;
-  const int m0 = it.mt * BM;
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int m0 = mt * BM;
   if (m0 >= len) return;
   const int g = h / p.G;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -461,10 +392,11 @@ attn_fp8_kernel(AttnParams p) {
   // explicit wait + barrier below orders each buffer's copy before its reads.
   __shared__ __attribute__((aligned(1024))) uint8_t kvl[4 * TB];
 
-  WorkItem it;
-  if (!decode_work<BM>(p, it)) return;
-  const int h = it.h, seq0 = it.seq0, len = it.len;
-  const int m0 = it.mt * BM;
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int m0 = mt * BM;
   if (m0 >= len) return;
   const int g = h / p.G;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
@@ -667,10 +599,11 @@ attn_fwd_f32_kernel(AttnParams p) {
   const float* __restrict__ q = static_cast<const float*>(p.q);
   const float* __restrict__ k = static_cast<const float*>(p.k);
   const float* __restrict__ v = static_cast<const float*>(p.v);
-  WorkItem it;
-  if (!decode_work<64>(p, it)) return;
-  const int h = it.h, seq0 = it.seq0, len = it.len;
-  const int m0 = it.mt * 64;
+  int b, h, mt;
+  if (!decode_work(p, b, h, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int m0 = mt * 64;
   if (m0 >= len) return;
   const int g = h / p.G;
   const int qi = m0 + threadIdx.x;
@@ -720,11 +653,11 @@ attn_fwd_f32_kernel(AttnParams p) {
 
 template <int D, bool CAUSAL, int OUT>
 static void launch_typed(const AttnArgs& a, AttnParams& p, hipStream_t stream) {
-  // one workgroup per query tile of every head and sample under the host
-  // bound max_seqlen, rounded up to whole rounds of the 8 XCDs
   const int bm = a.in_dtype == LITEVLM_F32 ? 64 : 128;
-  const long long n_work = (long long)((a.max_seqlen + bm - 1) / bm) * a.Hq * a.B;
-  const dim3 grid((unsigned)(8 * ((n_work + 7) / 8)));
+  p.n_mtiles = (a.max_seqlen + bm - 1) / bm;
+  p.n_work = p.n_mtiles * a.Hq * a.B;
+  p.per_xcd = (p.n_work + 7) / 8;
+  const dim3 grid(8 * p.per_xcd);
   if (a.in_dtype == LITEVLM_BF16)
     hipLaunchKernelGGL((attn_bf16_kernel<D, CAUSAL, OUT>), grid, dim3(256), 0, stream, p);
   else if (a.in_dtype == LITEVLM_FP8_E4M3)
