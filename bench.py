@@ -87,9 +87,18 @@ def source_hash(path):
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
+def kernel_base(name):
+    """'void litevlm::attn_bf16_kernel<128, true, 1>(...)' -> 'attn_bf16_kernel<128, true, 1>'."""
+    n = name.split("(", 1)[0]
+    if n.startswith("void "):
+        n = n[5:]
+    return n.split("litevlm::", 1)[1] if "litevlm::" in n else n
+
+
 def kernel_source(name):
+    base = kernel_base(name)
     for prefix, src in KERNEL_SOURCES:
-        if name.startswith(prefix):
+        if base.startswith(prefix):
             return src
     return None
 
@@ -134,8 +143,8 @@ def traffic_reduce(fa, wa, fc, wc, mb, out):
     counter scaled by (known bytes / measured) of the calibration copy."""
     known = int(mb * 1e6) // 4 * 4
     fetch, write = _per_dispatch(fa, "FETCH_SIZE"), _per_dispatch(wa, "WRITE_SIZE")
-    cf = [v for k, v in _per_dispatch(fc, "FETCH_SIZE").items() if "elementwise" in k]
-    cw = [v for k, v in _per_dispatch(wc, "WRITE_SIZE").items() if "elementwise" in k]
+    cf = [v for k, v in _per_dispatch(fc, "FETCH_SIZE").items() if "_add<" in k]
+    cw = [v for k, v in _per_dispatch(wc, "WRITE_SIZE").items() if "_add<" in k]
     if not cf or not cw:
         raise SystemExit("no elementwise copy dispatches in the calibration files")
     kf = known / (cf[0][0] * 1024.0)
@@ -148,7 +157,7 @@ def traffic_reduce(fa, wa, fc, wc, mb, out):
             continue
         f_kib, n_f = fetch[name]
         w_kib, n_w = write[name]
-        rec["kernels"][name] = {
+        rec["kernels"][kernel_base(name)] = {
             "fetch_kib_per_dispatch": f_kib, "write_kib_per_dispatch": w_kib, "dispatches": [n_f, n_w],
             "hbm_bytes_per_launch": round(f_kib * 1024.0 * kf + w_kib * 1024.0 * kw),
             "source": src, "source_sha256_16": source_hash(os.path.join(CSRC, src))}
