@@ -326,10 +326,14 @@ constexpr int kFlagsPer = kMaxSplitTiles / kSweepWaves;
 
 __device__ __forceinline__ void load_keep_bytes(const uint8_t* keep_row, int tile0, int V_full, int w, int lane,
                                                 uint8_t f[kFlagsPer]) {
+  // unconditional loads (of valid bytes when there is no mask): a branch here
+  // would make the compiler wait for every load in flight
+  const bool masked = keep_row && V_full > 0;
 #pragma unroll
   for (int i = 0; i < kFlagsPer; ++i) {
     const int key = (tile0 + w + kSweepWaves * i) * KB + lane;
-    f[i] = (keep_row && V_full > 0) ? keep_row[min(key, V_full - 1)] : 1;
+    const uint8_t* fp = masked ? keep_row + min(key, V_full - 1) : nullptr;
+    f[i] = masked ? *fp : 1;
   }
 }
 
@@ -790,14 +794,27 @@ struct QRing {
   }
 };
 
+// One float2 store to LDS (ds_write_b64), opaque to the compiler's wait
+// insertion; the caller orders it with an LDS wait and a barrier.
+__device__ __forceinline__ void lds_store_f2(float2* p, float2 v) {
+  const uint32_t a = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) float2*)p);
+  asm volatile("ds_write_b64 %0, %1" ::"v"(a), "v"(v) : "memory");
+}
+
 // Workgroup-wide OR through four per-wave words of the kernel's own LDS
 // array (the runtime's block reduction would add an LDS object of its own).
+// The store and the barriers wait for LDS accesses only (direct copies into
+// other LDS buffers may stay in flight).
 __device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
   const uint64_t m = __ballot(v);
-  if ((threadIdx.x & 63) == 0) slots[threadIdx.x >> 6] = m != 0;
-  __syncthreads();
+  if ((threadIdx.x & 63) == 0) {
+    const uint32_t a = (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint32_t*)(slots + (threadIdx.x >> 6)));
+    const uint32_t x = m != 0 ? 1u : 0u;
+    asm volatile("ds_write_b32 %0, %1" ::"v"(a), "v"(x) : "memory");
+  }
+  lds_barrier();
   const bool r = (slots[0] | slots[1] | slots[2] | slots[3]) != 0;
-  __syncthreads();
+  lds_barrier();
   return r;
 }
 
@@ -862,8 +879,14 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
       for (int j = 0; j < 8; ++j) pre[h][j] = rp[(size_t)min(p + (8 * h + j) * P, d.ns1 - 1) * d.R];
   }
 
-  // The keys, the first two chunks and the keep byte of the thread's key are
-  // in flight while the row statistics are merged.
+  // The keep byte of the thread's key, the keys and the first two query
+  // chunks are in flight while the row statistics are merged (loads complete
+  // in order: the keep byte first, since the merge is followed by its use).
+  const int tkey = vt * KT + tid;
+  // an unconditional load (of a valid byte when there is no mask), so that no
+  // branch makes the compiler wait for every load in flight here
+  const uint8_t* tkp = keep_row ? keep_row + min(tkey, d.V_full - 1) : static_cast<const uint8_t*>(kv);
+  const uint8_t tkraw = *tkp;
   Ring ring;
   ring.init(q, b, g, d, w, lane, row0, cstep);
   Tile tile;
@@ -872,9 +895,6 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
                  (size_t)d.Hkv * Tile::RB, max(0, min(KW, d.V_full - key0)), lane);
   ring.issue(lds, w);
   if (nch > 1) ring.issue(lds + Ring::CB, w);
-  asm volatile("" ::: "memory");  // keep the copies ahead of the keep-byte load
-  const int tkey = vt * KT + tid;
-  const uint8_t tkb = keep_row ? keep_row[min(tkey, d.V_full - 1)] : 1;
 
   // fold splits s0 + j*P (j < 8; those past ns1 ignored) into a running (max, sum)
   auto fold8 = [&](float2 (&u)[8], int s0, float& m, float& z) {
@@ -886,9 +906,9 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
     }
     if (mg != -INFINITY) {
       // exp2(-inf - mg) = 0 for splits without a visible key (their sum is 0)
-      z = m == -INFINITY ? 0.f : z * exp2f(m - mg);
+      z = m == -INFINITY ? 0.f : z * __builtin_amdgcn_exp2f(m - mg);
 #pragma unroll
-      for (int j = 0; j < 8; ++j) z += u[j].y * exp2f(u[j].x - mg);
+      for (int j = 0; j < 8; ++j) z += u[j].y * __builtin_amdgcn_exp2f(u[j].x - mg);
       m = mg;
     }
   };
@@ -916,13 +936,20 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
     for (int off = 1; off < P; off <<= 1) {
       const float mo = __shfl_xor(m, off), zo = __shfl_xor(z, off);
       const float mn = fmaxf(m, mo);
-      z = (m == -INFINITY ? 0.f : z * exp2f(m - mn)) + (mo == -INFINITY ? 0.f : zo * exp2f(mo - mn));
+      z = (m == -INFINITY ? 0.f : z * __builtin_amdgcn_exp2f(m - mn)) +
+          (mo == -INFINITY ? 0.f : zo * __builtin_amdgcn_exp2f(mo - mn));
       m = mn;
     }
-    // rows past R: exp2(-inf) = 0 and a zero weight
-    if (p == 0 && lr < nrows) table[lr] = r < d.R ? make_float2(-m, 1.0f / z) : make_float2(-INFINITY, 0.f);
+    // rows past R: exp2(-inf) = 0 and a zero weight. The store is written as
+    // inline assembly: the table and the chunk buffers being filled by the
+    // direct copies are disjoint, but the compiler cannot tell and would make
+    // the store wait for every copy in flight.
+    if (p == 0 && lr < nrows) {
+      const float2 e = r < d.R ? make_float2(-m, 1.0f / z) : make_float2(-INFINITY, 0.f);
+      lds_store_f2(table + lr, e);
+    }
   }
-
+  const uint8_t tkb = keep_row ? tkraw : 1;
   const bool tkept = tkey < d.V_full && tkb != 0;
   if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds + FLG))) {
     // no kept key in the tile: nothing to add (the copies into LDS land
@@ -1004,7 +1031,8 @@ constexpr int kTopkThreads = 1024;
 constexpr int kTopkWaves = kTopkThreads / 64;
 constexpr int kDigitBits = 12;              // radix digit width of the selection
 constexpr int kBins = 1 << kDigitBits;
-static_assert(kBins == 4 * kTopkThreads, "each thread owns four histogram bins");
+constexpr int kBinsPer = kBins / kTopkThreads;  // histogram bins owned by each thread
+static_assert(kBins == kBinsPer * kTopkThreads, "the threads own whole runs of histogram bins");
 static_assert(LITEVLM_MAX_VISUAL % (4 * kTopkThreads) == 0, "key loads come in whole rounds of float4");
 
 __device__ __forceinline__ int wave_sum_int(int v) {
@@ -1082,16 +1110,11 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   const int T = S - V_full;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
 
-  // Kept-visual counts of samples 0..b, one sample per wave at a time.
-  for (int bb = wave; bb <= b; bb += kTopkWaves) {
-    const int c = token_keep ? wave_count_flags(token_keep + (size_t)bb * S, V_full, lane) : V_full;
-    if (lane == 0) vcnt[bb] = c;
-  }
-  for (int i = tid; i < kBins; i += kTopkThreads) hist[i] = 0;
-
   // Order keys of the kept tokens' scores (dropped tokens: key 0; kept keys
-  // are >= 0x80000000 since scores are >= 0); loads are unconditional from
-  // clamped addresses so that a thread's rounds are all in flight at once.
+  // are >= 0x80000000 since scores are >= 0). The column sums and keep bytes
+  // of this sample are requested first, from clamped addresses, so that a
+  // thread's rounds are all in flight at once, together with the loads of the
+  // kept-visual counts below.
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * S : nullptr;
   const unsigned long long* ac = acc + (size_t)b * V_full;
   float* sc = scores + (size_t)b * V_full;
@@ -1100,18 +1123,32 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   const bool vec = V_full >= 4 && (V_full & 3) == 0 && (reinterpret_cast<uintptr_t>(sc) & 15) == 0 &&
                    (reinterpret_cast<uintptr_t>(ac) & 15) == 0 &&
                    (keep_row == nullptr || (reinterpret_cast<uintptr_t>(keep_row) & 3) == 0);
+  typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
+  constexpr int R4 = LITEVLM_MAX_VISUAL / (4 * kTopkThreads);
+  u64x2 a4[R4][2];
+  uint32_t f4[R4];
   if (vec) {
-    typedef unsigned long long u64x2 __attribute__((ext_vector_type(2)));
-    constexpr int R4 = LITEVLM_MAX_VISUAL / (4 * kTopkThreads);
-    u64x2 a4[R4][2];
-    uint32_t f4[R4];
 #pragma unroll
     for (int i = 0; i < R4; ++i) {
       const int j4 = min(4 * (tid + i * kTopkThreads), V_full - 4);
       a4[i][0] = *reinterpret_cast<const u64x2*>(ac + j4);
       a4[i][1] = *reinterpret_cast<const u64x2*>(ac + j4 + 2);
-      f4[i] = keep_row ? *reinterpret_cast<const uint32_t*>(keep_row + j4) : 0x01010101u;
+      // unconditional load (of valid bytes when there is no mask): no branch
+      const uint32_t* fp = keep_row ? reinterpret_cast<const uint32_t*>(keep_row + j4)
+                                    : reinterpret_cast<const uint32_t*>(ac + j4);
+      const uint32_t fraw = *fp;
+      f4[i] = keep_row ? fraw : 0x01010101u;
     }
+  }
+
+  // Kept-visual counts of samples 0..b, one sample per wave at a time.
+  for (int bb = wave; bb <= b; bb += kTopkWaves) {
+    const int c = token_keep ? wave_count_flags(token_keep + (size_t)bb * S, V_full, lane) : V_full;
+    if (lane == 0) vcnt[bb] = c;
+  }
+  for (int i = tid; i < kBins; i += kTopkThreads) hist[i] = 0;
+
+  if (vec) {
 #pragma unroll
     for (int i = 0; i < R4; ++i) {
       const int j4 = 4 * (tid + i * kTopkThreads);
@@ -1198,25 +1235,32 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
         }
       }
       __syncthreads();
-      // thread t owns bins 4t..4t+3; "above" counts candidates in higher bins
-      const int c0 = hist[4 * tid], c1 = hist[4 * tid + 1], c2 = hist[4 * tid + 2], c3 = hist[4 * tid + 3];
-      const int csum = c0 + c1 + c2 + c3;
+      // thread t owns bins kBinsPer*t ..; "above" counts candidates in higher bins
+      int cb[kBinsPer];
+      int csum = 0;
+#pragma unroll
+      for (int u = 0; u < kBinsPer; ++u) {
+        cb[u] = hist[kBinsPer * tid + u];
+        csum += cb[u];
+      }
       int total;
       const int excl = block_scan_excl(csum, wsum[1 + (pass & 1)], &total);
       const int above = total - excl - csum;
       // bins are cleared for the next pass by their owners
-      hist[4 * tid] = hist[4 * tid + 1] = hist[4 * tid + 2] = hist[4 * tid + 3] = 0;
+#pragma unroll
+      for (int u = 0; u < kBinsPer; ++u) hist[kBinsPer * tid + u] = 0;
       if (above < krem && above + csum >= krem) {
-        int a = above, dsel;
-        if (a + c3 >= krem) {
-          dsel = 4 * tid + 3;
-        } else if ((a += c3) + c2 >= krem) {
-          dsel = 4 * tid + 2;
-        } else if ((a += c2) + c1 >= krem) {
-          dsel = 4 * tid + 1;
-        } else {
-          a += c1;
-          dsel = 4 * tid;
+        // the bin holding the krem-th largest candidate, from the top bin down
+        int a = above, dsel = kBinsPer * tid;
+        bool found = false;
+#pragma unroll
+        for (int u = kBinsPer - 1; u >= 0; --u) {
+          if (!found && a + cb[u] >= krem) {
+            dsel = kBinsPer * tid + u;
+            found = true;
+          } else if (!found) {
+            a += cb[u];
+          }
         }
         sel_digit = dsel;
         sel_above = a;
