@@ -665,6 +665,25 @@ def main():
                           "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                           "attn_frac_bf16_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
 
+    # the same batch-1 shape in E4M3 across the keep ratios (FP8 beside FP16 in
+    # the prefill-latency comparison of Figure 3b)
+    sweep_fp8 = []
+    if not args.no_sweep:
+        rn8 = Runner([synth.config_case(3, dtype="fp8")])
+        for r in SWEEP:
+            m, p, c = rn8.measure(r, max(10, args.steps // 2), 3)
+            sl = np.diff(c).tolist()
+            f = attn_flops(sl, Hq, D)
+            sweep_fp8.append({"keep_ratio": r, "compacted_len": sl, "ms_per_step": round(m, 4),
+                              "patch_select_us": round(p[0] * 1e3, 2),
+                              "score_topk_gather_us": round(p[1] * 1e3, 2),
+                              "prefill_attn_us": round(p[2] * 1e3, 2),
+                              "attn_gflop": round(f / 1e9, 2),
+                              "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
+                              "attn_frac_fp8_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4)})
+        del rn8
+        torch.cuda.empty_cache()
+
     secondary, decode_lines, tsm_lines, psm_lines = [], [], [], []
     if not args.no_sweep:
         psm_lines.append(measure_psm(1, "text query of 128 tokens, batch 1"))
@@ -741,6 +760,7 @@ def main():
                      "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": traffic,
                      "flop_per_launch": fl},
         "sweep": sweep,
+        "sweep_fp8": sweep_fp8,
         "secondary": secondary,
         "decode": decode_lines,
         "tsm_front_end": tsm_lines,

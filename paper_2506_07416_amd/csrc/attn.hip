@@ -366,16 +366,17 @@ attn_bf16_kernel(AttnParams p) {
 // that a lane half's 32 accumulator values are keys 32*hl .. 32*hl+31, the B
 // operand of one P.V k-step. K rows are 16-byte pieces read directly; V is
 // row-major and read transposed with ds_read_b64_tr_b8 (8 keys per read).
-// P is quantised as p*2^8 under an exact running max: with the max exact every
-// p is <= 1, and the 2^8 shift keeps p >= 2^-14 out of the E4M3 subnormal
-// range (the lazy rescale of the bf16 path would let p reach 2^TAU, where the
-// coarser E4M3 steps cost accuracy).
+// P is quantised as p*2^8 under a running max that may lag the row max by at
+// most half a binade: every p is then <= 2^0.5, so p*2^8 <= 362 stays inside
+// the E4M3 range (448), and the 2^8 shift keeps p >= 2^-14 out of the E4M3
+// subnormal range. The output is rescaled only when a row's max grows by more
+// than that half binade, which after the first tiles of a row is rare.
 
 typedef int i32x2 __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i32x2 lds_i32x2;
 
 template <int D, bool CAUSAL, int OUT>
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(256, 3)
 attn_fp8_kernel(AttnParams p) {
   constexpr int BN = 64, NW = 4, BM = 128;
   constexpr int RB = D;                     // bytes per key row
@@ -385,6 +386,7 @@ attn_fp8_kernel(AttnParams p) {
   constexpr int NI = TB / 1024;             // wave copies per tile
   constexpr int QKS = D / 64, DB = D / 32;
   constexpr int PSHIFT = 8;
+  constexpr float TAU = 0.5f;               // log2 lag allowed between the running and the row max
   static_assert(TB % 1024 == 0, "tile must split into whole wave copies");
   // One LDS object holds both K and V double buffers (K at buf*TB, V at
   // (2+buf)*TB). With a single object the compiler adds no vmcnt wait of its
@@ -399,7 +401,8 @@ attn_fp8_kernel(AttnParams p) {
   const int m0 = mt * BM;
   if (m0 >= len) return;
   const int g = h / p.G;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches
   const int lq = lane & 31, hl = lane >> 5;
   const int g16 = lane >> 4, s16 = lane & 15;
   const uint32_t kvrow = (uint32_t)p.Hkv * RB;
@@ -482,8 +485,16 @@ attn_fp8_kernel(AttnParams p) {
   for (int db = 0; db < DB; ++db)
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
+  float m_run = -INFINITY;
+  // row sums by the matrix core: ones^T P^T puts the row sum of the quantised
+  // p in every accumulator row
+  f32x16 lsum;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) lsum[r] = 0.f;
+  const i32x8 ones = {0x38383838, 0x38383838, 0x38383838, 0x38383838,
+                      0x38383838, 0x38383838, 0x38383838, 0x38383838};  // E4M3 1.0
   const float c = p.scale_log2;
+  const float tau_raw = TAU / c;  // TAU in raw logit units (c > 0)
   const int kend = CAUSAL ? min(len, m0 + BM) : len;
   const int nt = (kend + BN - 1) / BN;
 
@@ -529,12 +540,13 @@ attn_fp8_kernel(AttnParams p) {
         const float2 pr = pair_xor32(mx);
         mx = __builtin_elementwise_maximum(pr.x, pr.y);
       }
-      // exact running max: rescale whenever it grows
-      const bool grow = mx > m_run;
+      // lazy running max: rescale only when a row's max grows past m + TAU
+      const bool grow = mx > m_run + tau_raw;
       if (__any(grow)) {
         const float m_new = grow ? mx : m_run;
         const float alpha = grow ? __builtin_amdgcn_exp2f((m_run - m_new) * c) : 1.f;
-        l_run *= alpha;
+#pragma unroll
+        for (int r = 0; r < 16; ++r) lsum[r] *= alpha;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -543,7 +555,6 @@ attn_fp8_kernel(AttnParams p) {
       }
       // p * 2^PSHIFT = exp2(s*c - m*c + PSHIFT)
       const float mc = (m_run == -INFINITY) ? 0.f : m_run * c - (float)PSHIFT;
-      float rsi[8];
       int pw[8];
 #pragma unroll
       for (int i = 0; i < 8; ++i) {
@@ -551,12 +562,11 @@ attn_fp8_kernel(AttnParams p) {
         float e[4];
 #pragma unroll
         for (int u = 0; u < 4; ++u) e[u] = __builtin_amdgcn_exp2f(fmaf(s[nb][r0 + u], c, -mc));
-        rsi[i] = (e[0] + e[1]) + (e[2] + e[3]);
         int wd = __builtin_amdgcn_cvt_pk_fp8_f32(e[0], e[1], 0, false);
         pw[i] = __builtin_amdgcn_cvt_pk_fp8_f32(e[2], e[3], wd, true);
       }
-      l_run += ((rsi[0] + rsi[1]) + (rsi[2] + rsi[3])) + ((rsi[4] + rsi[5]) + (rsi[6] + rsi[7]));
       const i32x8 pb = {pw[0], pw[1], pw[2], pw[3], pw[4], pw[5], pw[6], pw[7]};
+      lsum = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(ones, pb, lsum, 0, 0, 0, 0, 0, 0);
       const uint8_t* vl = kvl + (2 + BUF) * TB;
 #pragma unroll
       for (int db = 0; db < DB; ++db) {
@@ -577,7 +587,7 @@ attn_fp8_kernel(AttnParams p) {
     if (t + 1 < nt) step(t + 1, std::integral_constant<int, 1>{});
   }
 
-  const float l = sum_xor32(l_run);
+  const float l = lsum[0];
   const float inv = (l > 0.f) ? p.out_scale / l : 0.f;   // l already carries 2^PSHIFT
   if (qi < len) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
