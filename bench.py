@@ -543,7 +543,13 @@ def main():
         T = c.S - c.V_full
         kept = int(nv.sum().item()) + c.B * T
         fl_alg = 2.0 * Dm * (kept * c.Hkv * c.D + c.B * T * c.Hq * c.D)
-        fl_done = 2.0 * Dm * (c.B * c.S * c.Hkv * c.D + c.B * T * c.Hq * c.D)
+        # key rows the kernel computes: its row tiles (256 rows when that tile
+        # still gives every CU a workgroup, else 128) holding at least one kept token
+        mt = 256 if (c.Hkv * c.D) % 256 == 0 and c.B * ((c.S + 255) // 256) * (c.Hkv * c.D // 256) >= 256 else 128
+        keep_np = tk.cpu().numpy()
+        krows = sum(min(mt, c.S - r0) for bb in range(c.B) for r0 in range(0, c.S, mt)
+                    if keep_np[bb, r0:r0 + mt].any())
+        fl_done = 2.0 * Dm * (krows * c.Hkv * c.D + c.B * T * c.Hq * c.D)
         cpu_ms = None
         if cfg == 3:
             def tsm_oracle():
@@ -558,7 +564,8 @@ def main():
                 "tflops": round(fl_alg / (us * 1e-6) / 1e12, 1),
                 "frac_bf16_peak": round(fl_alg / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
                 "note": "keys of the kept tokens and queries of the text tokens count as algorithmic; "
-                        "the kernel also projects the keys of dropped views' tokens",
+                        "the kernel skips row tiles of dropped tokens only, so a tile that mixes kept "
+                        "and dropped rows is computed whole",
                 "gather_hidden": {"keep_ratio": r, "rows": rows, "us": round(g_us, 2),
                                   "gbs": round(g_bytes / (g_us * 1e-6) / 1e9, 1),
                                   "frac_hbm": round(g_bytes / (g_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)}}

@@ -272,7 +272,7 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
  * its queries and keys from RMS-normalised hidden states through bias-free
  * projections and rotary position embeddings:
  *   r_j      = 1 / sqrt(mean_c x[b,j,c]^2 + eps)
- *   k[b,j,h] = rope(r_j * (x[b,j] . W_k'[h*D:(h+1)*D]), pos_j)   for every token j
+ *   k[b,j,h] = rope(r_j * (x[b,j] . W_k'[h*D:(h+1)*D]), pos_j)   for every kept token j
  *   q[b,t,h] = rope(r_t * (x[b,t] . W_q'[h*D:(h+1)*D]), pos_t)   for the text tokens t
  *   rope pairs element d < D/2 of a head with element d + D/2 and rotates the
  *   pair by the angle pos * rope_theta^(-2d/D);
@@ -293,7 +293,9 @@ litevlm_status_t litevlm_prefill_attn(int32_t in_dtype, int32_t out_dtype, int32
  *   rope_theta         rotary base (finite, > 1)
  *   q                  dev out bf16 [B, S, Hq, D]: rows V_full..S-1 of every sample are
  *                      written, the visual rows are left untouched
- *   k                  dev out bf16 [B, S, Hkv, D]: every row written
+ *   k                  dev out bf16 [B, S, Hkv, D]: the rows of kept tokens are written
+ *                      (every row when token_keep is NULL); the rows of dropped tokens
+ *                      are left untouched, since the scoring never reads them
  */
 litevlm_status_t litevlm_tsm_qk(int32_t B, int32_t S, int32_t V_full, int32_t Dm, int32_t Hq, int32_t Hkv,
                                 int32_t D, const void* hidden, const uint8_t* token_keep, const void* w_q,

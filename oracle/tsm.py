@@ -18,8 +18,8 @@ taken here are the decoder family's standard ones:
 * Positions are those of the patch-selected sequence: tokens of dropped views
   do not exist, so a token's position is the number of kept tokens before it.
 
-Only the rows the scoring reads are produced: keys for every token, queries
-for the text tokens.
+The keys are produced for every token (the scoring reads those of the kept
+tokens only) and the queries for the text tokens.
 """
 from __future__ import annotations
 

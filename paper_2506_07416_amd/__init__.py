@@ -209,9 +209,10 @@ def tsm_fold_gain(w: torch.Tensor, gamma: torch.Tensor, out: Optional[torch.Tens
 def tsm_qk(hidden: torch.Tensor, token_keep: Optional[torch.Tensor], V_full: int, w_q: torch.Tensor,
            w_k: torch.Tensor, Hq: int, Hkv: int, D: int, eps: float = 1e-5, rope_theta: float = 1e6,
            q: Optional[torch.Tensor] = None, k: Optional[torch.Tensor] = None):
-    """Scoring queries (text rows) and keys (all rows) of the Token Selection
+    """Scoring queries (text rows) and keys (kept rows) of the Token Selection
     Module from bf16 hidden states [B,S,Dm]; w_q/w_k carry the folded RMS gain.
-    Returns (q [B,S,Hq,D], k [B,S,Hkv,D]) in bf16; q's visual rows are untouched."""
+    Returns (q [B,S,Hq,D], k [B,S,Hkv,D]) in bf16; q's visual rows and the key
+    rows of dropped tokens are untouched."""
     B, S, Dm = hidden.shape
     dev = hidden.device
     q = q if q is not None else torch.empty((B, S, Hq, D), dtype=torch.bfloat16, device=dev)

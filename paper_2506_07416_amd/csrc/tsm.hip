@@ -1,7 +1,7 @@
 // Token Selection Module front end: the scoring queries and keys of the
 // standalone first decoder layer, from the layer's input hidden states.
 //
-//   k[b, j]   = rope(r_j * x[b, j] W_k'^T, pos_j)   for every token j
+//   k[b, j]   = rope(r_j * x[b, j] W_k'^T, pos_j)   for every kept token j
 //   q[b, t]   = rope(r_t * x[b, t] W_q'^T, pos_t)   for the text tokens t
 //   r_j       = 1 / sqrt(mean_c x[b, j, c]^2 + eps)  (RMS normalisation)
 //   pos_j     = number of kept tokens before j (positions of the patch-selected sequence)
@@ -46,7 +46,8 @@ struct TsmTile {
   static constexpr int kBB = NT * kRowB;  // B tile bytes per stage
   static constexpr int kStageB = kAB + kBB;
   static constexpr int kRingB = kStages * kStageB;
-  static constexpr int kLdsB = kRingB + MT * 4 /* row factors */ + MT * 4 /* positions */ + 128 /* reductions */;
+  static constexpr int kLdsB =
+      kRingB + MT * 4 /* row factors */ + MT * 4 /* positions */ + 128 /* reductions */ + MT /* keep flags */;
   static constexpr int kWgPerCu = (160 * 1024 / kLdsB) >= 2 ? 2 : 1;
   static constexpr int kThreads = 64 * NW;
   static constexpr int kNWR = MT / 64;       // waves along the rows
@@ -133,6 +134,7 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
   float* rs = reinterpret_cast<float*>(lds + kRingB);
   int* pos = reinterpret_cast<int*>(lds + kRingB + kMT * 4);
   int* red = reinterpret_cast<int*>(lds + kRingB + kMT * 8);
+  uint8_t* kflag = lds + kRingB + kMT * 8 + 128;
 
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wr = w % NWR, wc = w / NWR, hl = lane >> 5, l32 = lane & 31;
@@ -167,7 +169,10 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
       __syncthreads();
       int before = t0 == 0 ? 0 : red[2 * NW];  // kept rows of the earlier chunks
       for (int x = 0; x < w; ++x) before += red[NW + x];
-      if (t < kMT) pos[t] = base + before + (incl - f);
+      if (t < kMT) {
+        pos[t] = base + before + (incl - f);
+        kflag[t] = (uint8_t)f;
+      }
       __syncthreads();
       if (tid == 0) {
         int c = t0 == 0 ? 0 : red[2 * NW];
@@ -175,6 +180,13 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
         red[2 * NW] = c;
       }
     }
+  }
+
+  // ---- a key tile whose rows are all dropped tokens produces nothing: the
+  // keys of dropped views are never scored
+  if (!isq && p.keep) {
+    __syncthreads();
+    if (red[2 * NW] == 0) return;
   }
 
   // ---- per-lane copy sources (fixed) and operand offsets (fixed)
@@ -321,7 +333,7 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = 64 * wr + 32 * rb + acc_row(r, hl);
-        if (row < nrows) {
+        if (row < nrows && (isq || kflag[row])) {
           const float f = rs[row];
           const float x1 = acc[rb][c][r] * f, x2 = acc[rb][cp][r] * f;
           // angle pos * theta^(-2d/D), reduced to [-pi, pi] in double

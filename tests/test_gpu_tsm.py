@@ -5,7 +5,11 @@ The oracle takes the gain and the unfolded weights in float64; the GPU folds
 the gain into bf16 weights and rounds its outputs to bf16, so the comparison
 allows for bf16 rounding: |got - ref| <= 1e-2 + 2e-2*|ref| elementwise and a
 per-(row, head) relative L2 error of at most 1e-2 (bf16 output rounding alone
-gives about 2e-3, the folded-weight rounding about as much again)."""
+gives about 2e-3, the folded-weight rounding about as much again).
+
+Key rows are compared for the kept tokens; the kernel leaves the key rows of
+dropped tokens untouched, which is checked against a sentinel written before
+the call."""
 import numpy as np
 import pytest
 import torch
@@ -20,6 +24,7 @@ pytestmark = pytest.mark.gpu
 
 EPS, THETA = 1e-5, 1e6
 TSM_RTOL, TSM_ATOL, TSM_ROW_L2 = 2e-2, 1e-2, 1e-2
+SENTINEL = 0x7FA5  # a bf16 NaN payload no computed key row holds
 
 
 def run(case, Dm, seed, eps=EPS, theta=THETA, use_keep=True):
@@ -35,14 +40,18 @@ def run(case, Dm, seed, eps=EPS, theta=THETA, use_keep=True):
     g = torch.from_numpy(gamma).cuda()
     wq_f = lv.tsm_fold_gain(to_device(wq, "bf16"), g)
     wk_f = lv.tsm_fold_gain(to_device(wk, "bf16"), g)
-    q, k = lv.tsm_qk(to_device(hid, "bf16"), tk, V, wq_f, wk_f, Hq, Hkv, D, eps=eps, rope_theta=theta)
+    k0 = torch.full((B, S, Hkv, D), SENTINEL, dtype=torch.int16, device="cuda").view(torch.bfloat16)
+    q, k = lv.tsm_qk(to_device(hid, "bf16"), tk, V, wq_f, wk_f, Hq, Hkv, D, eps=eps, rope_theta=theta, k=k0)
     torch.cuda.synchronize()
     if tk is not None:
         assert np.array_equal(tk.cpu().numpy(), keep_ref)
+    kept = keep_ref.astype(bool)
+    kbits = k.cpu().view(torch.int16).numpy()
+    assert (kbits[~kept] == SENTINEL).all(), "key rows of dropped tokens were written"
     dec = oracle.litevlm.decode_stored
     qr, kr = OT.tsm_qk(dec(hid, "bf16"), keep_ref, V, gamma.astype(np.float64), dec(wq, "bf16"),
                        dec(wk, "bf16"), Hq, Hkv, D, eps, theta)
-    return to_float64(q[:, V:]), to_float64(k), qr, kr
+    return to_float64(q[:, V:]), to_float64(k.cpu()[torch.from_numpy(kept)]), qr, kr[kept]
 
 
 def check(got, ref, what):
