@@ -464,28 +464,45 @@ __global__ __launch_bounds__(kDecThreads) void decode_combine_kernel(DecodeParam
   __shared__ float4 racc[SLOTS][V4];
   __shared__ float rl[SLOTS];
 
+  // The first R splits of the thread's slot are requested together with their
+  // statistics before the maximum is known (addresses clamped to the last
+  // split, so every load is valid and none waits on a branch); splits beyond
+  // R*SLOTS, for very long caches, are read after it.
+  constexpr int R = 8;
+  const int slot = tid / V4, c = tid % V4;
+  float2 mr[R];
+  float4 xr[R];
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int s = min(slot + i * SLOTS, ns - 1);
+    mr[i] = ml[s];
+    xr[i] = po[(int64_t)s * V4 + c];
+  }
   float m = -INFINITY;
-  for (int s = tid; s < ns; s += kDecThreads) m = fmaxf(m, ml[s].x);
+#pragma unroll
+  for (int i = 0; i < R; ++i) m = fmaxf(m, mr[i].x);  // clamped repeats change no maximum
+  for (int s = slot + R * SLOTS; s < ns; s += SLOTS) m = fmaxf(m, ml[s].x);
 #pragma unroll
   for (int x = 1; x < kWave; x <<= 1) m = wave_max_xor(m, x);
   if (lane == 0) wmax[w] = m;
   __syncthreads();
   m = fmaxf(fmaxf(wmax[0], wmax[1]), fmaxf(wmax[2], wmax[3]));
 
-  const int slot = tid / V4, c = tid % V4;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float l = 0.f;
-#pragma unroll 4
-  for (int s = slot; s < ns; s += SLOTS) {
-    const float2 st = ml[s];
-    const float4 x = po[(int64_t)s * V4 + c];
+  auto add = [&](const float2 st, const float4 x) __attribute__((always_inline)) {
     const float wgt = __builtin_amdgcn_exp2f(st.x - m);
     l = fmaf(st.y, wgt, l);
     acc.x = fmaf(x.x, wgt, acc.x);
     acc.y = fmaf(x.y, wgt, acc.y);
     acc.z = fmaf(x.z, wgt, acc.z);
     acc.w = fmaf(x.w, wgt, acc.w);
-  }
+  };
+#pragma unroll
+  for (int i = 0; i < R; ++i)
+    if (slot + i * SLOTS < ns) add(mr[i], xr[i]);
+#pragma unroll 4
+  for (int s = slot + R * SLOTS; s < ns; s += SLOTS) add(ml[s], po[(int64_t)s * V4 + c]);
   racc[slot][c] = acc;
   if (c == 0) rl[slot] = l;
   __syncthreads();
