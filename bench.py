@@ -1,8 +1,10 @@
 """Benchmark of the LiteVLM select + prefill path on one MI355X.
 
-One step = the whole path on one batch: litevlm_patch_select ->
-litevlm_token_score_topk (scores, top-k, gather) -> litevlm_prefill_attn, all
-on one stream with no host synchronisation in between. The workload is the
+One step = the whole path on one batch: litevlm_select_score_topk (view
+selection inside the scoring kernels, scores, top-k, gather) ->
+litevlm_prefill_attn, all on one stream with no host synchronisation in
+between; the same steps with litevlm_patch_select as its own call before
+litevlm_token_score_topk are reported beside them. The workload is the
 6-view x 1024-visual-token + 128-text-token multi-camera prompt (GQA 32/8
 heads, head dim 128, bf16, batch 1) at keep ratio 0.5; the keep-ratio sweep
 {1.0, 0.5, 0.25} is reported alongside.
@@ -315,10 +317,14 @@ def main():
         return torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(dev)
 
     class Runner:
-        """Preallocated buffers and the three calls of one select + prefill step."""
+        """Preallocated buffers and the calls of one select + prefill step:
+        litevlm_select_score_topk (the patch selection inside the scoring call)
+        then litevlm_prefill_attn, or, unfused (always with query_rows),
+        litevlm_patch_select, the scoring call, then the attention."""
 
-        def __init__(self, cases, query_rows=None):
+        def __init__(self, cases, query_rows=None, fused=None):
             self.query_rows = query_rows
+            self.fused = (query_rows is None) if fused is None else fused
             self.sets = [dict(case=c, q=up(c.q, c.dtype), k=up(c.k, c.dtype), v=up(c.v, c.dtype),
                               logit=torch.from_numpy(c.view_logit).to(dev)) for c in cases]
             c = cases[0]
@@ -331,6 +337,8 @@ def main():
                              qc=torch.empty((B * S, Hq, D), dtype=t, device=dev),
                              kc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
                              vc=torch.empty((B * S, Hkv, D), dtype=t, device=dev),
+                             view_keep=torch.empty((B, c.N), dtype=torch.uint8, device=dev),
+                             n_visual_kept=torch.empty((B,), dtype=torch.int32, device=dev),
                              workspace=torch.empty((lv.workspace_bytes(B, S, V, Hq, Hkv, D, query_rows),),
                                                    dtype=torch.uint8, device=dev))
             self.o = torch.empty((B * S, Hq, D), dtype=torch.bfloat16, device=dev)
@@ -339,12 +347,19 @@ def main():
             c = self.case
             if ev is not None:
                 ev[0].record(stream)
-            _, tk, _ = lv.patch_select(st["logit"], c.view_offsets, c.S, c.w_lexical, c.threshold)
-            if ev is not None:
-                ev[1].record(stream)
-            lv.token_score_topk(st["q"], st["k"], st["v"], tk, r, c.V_full, q_scale=c.q_scale,
-                                k_scale=c.k_scale, v_scale=c.v_scale, out=self.outs,
-                                query_rows=self.query_rows)
+            if self.fused:
+                lv.select_score_topk(st["logit"], c.view_offsets, st["q"], st["k"], st["v"], r, c.V_full,
+                                     w_lexical=c.w_lexical, threshold=c.threshold, q_scale=c.q_scale,
+                                     k_scale=c.k_scale, v_scale=c.v_scale, token_keep=False, out=self.outs)
+                if ev is not None:
+                    ev[1].record(stream)
+            else:
+                _, tk, _ = lv.patch_select(st["logit"], c.view_offsets, c.S, c.w_lexical, c.threshold)
+                if ev is not None:
+                    ev[1].record(stream)
+                lv.token_score_topk(st["q"], st["k"], st["v"], tk, r, c.V_full, q_scale=c.q_scale,
+                                    k_scale=c.k_scale, v_scale=c.v_scale, out=self.outs,
+                                    query_rows=self.query_rows)
             if ev is not None:
                 ev[2].record(stream)
             lv.prefill_attn(self.outs["qc"], self.outs["kc"], self.outs["vc"], self.outs["cu_seqlens"],
@@ -381,7 +396,7 @@ def main():
             return total_ms / steps, per.mean(axis=0), cu
 
         def measure_graph(self, r, steps, warmup):
-            """ms per step with each input set's step (the three calls) captured
+            """ms per step with each input set's step (its calls) captured
             once in a HIP graph and the graphs replayed in rotation."""
             graphs = []
             for st in self.sets:
@@ -407,6 +422,15 @@ def main():
             ms = t0.elapsed_time(t1) / steps
             del graphs
             return ms
+
+    def call_us(rn, p):
+        """Per-call durations (us) of a step from measure()'s event pairs: fused,
+        the first pair is the whole select call and the second is empty."""
+        if rn.fused:
+            return {"patch_select_us": None, "select_call_us": round((p[0] + p[1]) * 1e3, 2),
+                    "prefill_attn_us": round(p[2] * 1e3, 2)}
+        return {"patch_select_us": round(p[0] * 1e3, 2), "select_call_us": round(p[1] * 1e3, 2),
+                "prefill_attn_us": round(p[2] * 1e3, 2)}
 
     def oracle_ms(fn, budget_s=3.0):
         """Median wall time of the CPU oracle call fn() (at least one run, about
@@ -653,10 +677,20 @@ def main():
     # written, and the gather's reads and writes
     sel_bytes = (B * T * Hq * D * esz + sum(v + T for v in V_b) * Hkv * D * esz + B * S
                  + 4 * B * V + 4 * sum(seqlens) + gbytes)
-    sel_us = per[1] * 1e3
+    sel_us = call_us(main_runner, per)["select_call_us"]
     traffic = measured_traffic("attn_bf16_kernel")
     sel_traffic = {k: measured_traffic(k) for k in ("score_rowstats", "score_colmass", "topk_compact",
                                                     "gather_rows")}
+
+    # the same steps with the patch selection as its own call before the scoring
+    unfused = None
+    if not args.no_sweep:
+        rn_u = Runner([st["case"] for st in main_runner.sets], fused=False)
+        m_u, p_u, _ = rn_u.measure(args.keep_ratio, args.steps, args.warmup)
+        unfused = {"ms_per_step": round(m_u, 4), **call_us(rn_u, p_u),
+                   "note": "litevlm_patch_select, litevlm_token_score_topk, litevlm_prefill_attn"}
+        del rn_u
+        torch.cuda.empty_cache()
 
     sweep = []
     if not args.no_sweep:
@@ -665,9 +699,7 @@ def main():
             sl = np.diff(c).tolist()
             f = attn_flops(sl, Hq, D)
             sweep.append({"keep_ratio": r, "compacted_len": sl, "ms_per_step": round(m, 4),
-                          "patch_select_us": round(p[0] * 1e3, 2),
-                          "score_topk_gather_us": round(p[1] * 1e3, 2),
-                          "prefill_attn_us": round(p[2] * 1e3, 2),
+                          **call_us(main_runner, p),
                           "attn_gflop": round(f / 1e9, 2),
                           "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                           "attn_frac_bf16_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)})
@@ -682,9 +714,7 @@ def main():
             sl = np.diff(c).tolist()
             f = attn_flops(sl, Hq, D)
             sweep_fp8.append({"keep_ratio": r, "compacted_len": sl, "ms_per_step": round(m, 4),
-                              "patch_select_us": round(p[0] * 1e3, 2),
-                              "score_topk_gather_us": round(p[1] * 1e3, 2),
-                              "prefill_attn_us": round(p[2] * 1e3, 2),
+                              **call_us(rn8, p),
                               "attn_gflop": round(f / 1e9, 2),
                               "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                               "attn_frac_fp8_peak": round(f / (p[2] * 1e-3) / 1e12 / PEAK_FP8_TFLOPS, 4)})
@@ -713,9 +743,7 @@ def main():
             peak = PEAK_FP8_TFLOPS if c.dtype == "fp8" else PEAK_BF16_TFLOPS
             secondary.append({"workload": "6 views x 1024 + 128 text, GQA 32/8, D=128, " + name,
                               "dtype": c.dtype, "compacted_len": sl, "ms_per_step": round(m, 4),
-                              "patch_select_us": round(p[0] * 1e3, 2),
-                              "score_topk_gather_us": round(p[1] * 1e3, 2),
-                              "prefill_attn_us": round(p[2] * 1e3, 2),
+                              **call_us(rn, p),
                               "attn_gflop": round(f / 1e9, 2),
                               "attn_tflops": round(f / (p[2] * 1e-3) / 1e12, 1),
                               "attn_frac_of_dtype_peak": round(f / (p[2] * 1e-3) / 1e12 / peak, 4)})
@@ -745,15 +773,17 @@ def main():
                    "keep_ratio": args.keep_ratio, "parallelism": "none (1 GPU)",
                    "input_sets_rotated": args.sets},
         "step_ms_p10_p50_p90": {"ms": [round(float(x), 4) for x in step_pct],
-                                "note": "per-step sums of the three calls' event-timed durations "
+                                "note": "per-step sums of the calls' event-timed durations "
                                         "(second pass; event records add small gaps)"},
         "hip_graph": {"ms_per_step": round(ms_graph, 4),
-                      "note": "the same steps with each input set's three calls captured in one HIP graph"},
+                      "note": "the same steps with each input set's calls captured in one HIP graph"},
         "prefill_attn_tflops": round(attn_tflops, 1),
-        "kernels_us": {"patch_select": round(per[0] * 1e3, 2),
-                       "token_score_topk_gather": round(per[1] * 1e3, 2),
-                       "prefill_attn": round(attn_us, 2)},
-        "select_stage": {"call": "litevlm_token_score_topk (score sweeps, top-k, gather)", "bound": "hbm",
+        "calls_us": {**call_us(main_runner, per),
+                     "note": "event-timed: litevlm_select_score_topk (view selection inside the scoring "
+                             "kernels, score sweeps, top-k, gather), then litevlm_prefill_attn"},
+        "unfused": unfused,
+        "select_stage": {"call": "litevlm_select_score_topk (view selection, score sweeps, top-k, gather)",
+                         "bound": "hbm",
                          "us": round(sel_us, 2), "algorithmic_bytes": sel_bytes,
                          "achieved": round(sel_bytes / (sel_us * 1e-6) / 1e9, 1), "peak": PEAK_HBM_GBS,
                          "unit": "GB/s", "frac": round(sel_bytes / (sel_us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),

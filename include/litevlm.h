@@ -8,7 +8,8 @@
  *   litevlm_psm_forward       the Patch Selection Module's view logits from the query
  *   litevlm_patch_select      view selection and per-view patch masking
  *   litevlm_token_score_topk  text-guided visual-token scoring, top-k, compaction
- *                             (litevlm_token_score_topk_rows: the last n text rows only)
+ *                             (litevlm_token_score_topk_rows: the last n text rows only;
+ *                             litevlm_select_score_topk: with the patch selection inside)
  *   litevlm_prefill_attn      causal GQA prefill attention over the compacted sequence
  * in front of the scoring, from the hidden states:
  *   litevlm_tsm_qk            the Token Selection Module's scoring queries and keys
@@ -167,6 +168,45 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
                                           double keep_ratio, float* scores, int32_t* kept_index,
                                           int32_t* cu_seqlens, void* qc, void* kc, void* vc,
                                           void* workspace, size_t workspace_bytes, void* stream);
+
+/* Most views litevlm_select_score_topk takes (the selection is taken inside
+ * every scoring workgroup, one comparison per view offset). */
+#define LITEVLM_MAX_FUSED_VIEWS 8
+
+/*
+ * litevlm_select_score_topk - litevlm_patch_select and litevlm_token_score_topk
+ * in one call: the scoring kernels take the view selection themselves from the
+ * view logits, so the step needs no token mask between the two.
+ *
+ * Paper: Design section, Patch Selection Module and Token Selection Module
+ * paragraphs (the selected views' patches are what the token scoring sees);
+ * the rest as for the two calls.
+ *
+ * The results are those of litevlm_patch_select (with these N, view offsets,
+ * logits, lexical scores, w_lexical and threshold) followed by
+ * litevlm_token_score_topk on its token mask, bit for bit: the same fp32
+ * decision, evaluated by the same device code.
+ *
+ *   N                  views, 1..LITEVLM_MAX_FUSED_VIEWS (N up to LITEVLM_MAX_VIEWS:
+ *                      LITEVLM_ERR_UNSUPPORTED; use the two calls)
+ *   view_offsets_host  host int32 [N+1]: view v holds visual positions
+ *                      [off[v], off[v+1]), off[0] = 0, non-decreasing, off[N] = V_full
+ *   view_logit, view_lexical, w_lexical, threshold   as for litevlm_patch_select
+ *   view_keep          dev out uint8 [B, N], or NULL
+ *   token_keep         dev out uint8 [B, S] (the token mask), or NULL
+ *   n_visual_kept      dev out int32 [B], or NULL
+ *   other arguments    as for litevlm_token_score_topk (the workspace size is
+ *                      litevlm_token_score_topk_workspace())
+ */
+litevlm_status_t litevlm_select_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                           int32_t Hkv, int32_t D, int32_t N, const int32_t* view_offsets_host,
+                                           const float* view_logit, const float* view_lexical, float w_lexical,
+                                           float threshold, const void* q, const void* k, const void* v,
+                                           float softmax_scale, float q_scale, float k_scale, float v_scale,
+                                           double keep_ratio, uint8_t* view_keep, uint8_t* token_keep,
+                                           int32_t* n_visual_kept, float* scores, int32_t* kept_index,
+                                           int32_t* cu_seqlens, void* qc, void* kc, void* vc, void* workspace,
+                                           size_t workspace_bytes, void* stream);
 
 /* Size of the device scratch array of litevlm_token_score_topk_noalloc (8 MiB
  * per GPU, held from the first such call on a GPU until the process ends). */

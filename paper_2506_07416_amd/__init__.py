@@ -23,7 +23,7 @@ import torch
 from . import _abi
 from ._abi import LiteVLMError, load  # noqa: F401
 
-__all__ = ["patch_select", "token_score_topk", "prefill_attn", "decode_attn", "tsm_qk", "tsm_fold_gain",
+__all__ = ["patch_select", "token_score_topk", "select_score_topk", "prefill_attn", "decode_attn", "tsm_qk", "tsm_fold_gain",
            "gather_hidden", "psm_forward",
            "dtype_code",
            "workspace_bytes", "decode_workspace_bytes", "LiteVLMError", "load"]
@@ -134,6 +134,52 @@ def token_score_topk(q: torch.Tensor, k: torch.Tensor, v: Optional[torch.Tensor]
         st = lib.litevlm_token_score_topk_rows(dtype_code(q.dtype), B, S, V_full, Hq, Hkv, D,
                                                int(query_rows), *common)
         _abi.check(st, "litevlm_token_score_topk_rows")
+    return o
+
+
+def select_score_topk(view_logit: torch.Tensor, view_offsets: Sequence[int], q: torch.Tensor,
+                      k: torch.Tensor, v: Optional[torch.Tensor], keep_ratio: float, V_full: int,
+                      w_lexical: float = 0.0, threshold: float = 0.5,
+                      view_lexical: Optional[torch.Tensor] = None, softmax_scale: Optional[float] = None,
+                      q_scale: float = 1.0, k_scale: float = 1.0, v_scale: float = 1.0, gather: bool = True,
+                      token_keep: bool = True, workspace: Optional[torch.Tensor] = None,
+                      out: Optional[dict] = None) -> dict:
+    """patch_select and token_score_topk in one call (litevlm_select_score_topk):
+    the returned dict holds token_score_topk's tensors plus view_keep [B,N],
+    n_visual_kept [B] and, when token_keep is set, the token mask [B,S]."""
+    lib = load()
+    B, S, Hq, D = q.shape
+    Hkv = k.shape[2]
+    N = view_logit.shape[1]
+    dev = q.device
+    if softmax_scale is None:
+        softmax_scale = 1.0 / math.sqrt(D)
+    o = dict(out or {})
+    o.setdefault("scores", torch.empty((B, V_full), dtype=torch.float32, device=dev))
+    o.setdefault("kept_index", torch.empty((B * S,), dtype=torch.int32, device=dev))
+    o.setdefault("cu_seqlens", torch.empty((B + 1,), dtype=torch.int32, device=dev))
+    o.setdefault("view_keep", torch.empty((B, N), dtype=torch.uint8, device=dev))
+    o.setdefault("n_visual_kept", torch.empty((B,), dtype=torch.int32, device=dev))
+    if token_keep:
+        o.setdefault("token_keep", torch.empty((B, S), dtype=torch.uint8, device=dev))
+    if gather:
+        o.setdefault("qc", torch.empty((B * S, Hq, D), dtype=q.dtype, device=dev))
+        o.setdefault("kc", torch.empty((B * S, Hkv, D), dtype=k.dtype, device=dev))
+        o.setdefault("vc", torch.empty((B * S, Hkv, D), dtype=v.dtype, device=dev))
+    nbytes = workspace_bytes(B, S, V_full, Hq, Hkv, D)
+    ws = workspace if workspace is not None else o.get("workspace")
+    if ws is None:
+        ws = torch.empty((max(nbytes, 1),), dtype=torch.uint8, device=dev)
+    o["workspace"] = ws
+    off = (ctypes.c_int32 * (N + 1))(*[int(x) for x in view_offsets])
+    st = lib.litevlm_select_score_topk(
+        dtype_code(q.dtype), B, S, V_full, Hq, Hkv, D, N, off, _ptr(view_logit), _ptr(view_lexical),
+        float(w_lexical), float(threshold), _ptr(q), _ptr(k), _ptr(v), float(softmax_scale), float(q_scale),
+        float(k_scale), float(v_scale), float(keep_ratio), _ptr(o["view_keep"]), _ptr(o.get("token_keep")),
+        _ptr(o["n_visual_kept"]), _ptr(o["scores"]), _ptr(o["kept_index"]), _ptr(o["cu_seqlens"]),
+        _ptr(o.get("qc")), _ptr(o.get("kc")), _ptr(o.get("vc")), _ptr(ws), ws.numel() * ws.element_size(),
+        _stream(dev))
+    _abi.check(st, "litevlm_select_score_topk")
     return o
 
 

@@ -16,6 +16,7 @@ OK, ERR_NULL_POINTER, ERR_BAD_SHAPE, ERR_BAD_VALUE, ERR_UNSUPPORTED, ERR_MISALIG
 F32, BF16, FP8_E4M3 = 0, 1, 2
 MAX_VIEWS, MAX_VISUAL, MAX_BATCH, MAX_HEADS = 64, 16384, 256, 128
 NOALLOC_SCRATCH_BYTES = 8 << 20
+MAX_FUSED_VIEWS = 8
 
 # Every symbol the header declares, with its C signature.
 _vp, _i32, _f32, _f64, _sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_float, ctypes.c_double, ctypes.c_size_t
@@ -34,6 +35,9 @@ SIGNATURES = {
     "litevlm_token_score_topk_rows": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp,
                                              _vp, _f32, _f32, _f32, _f32, _vp, _f64, _vp, _vp, _vp,
                                              _vp, _vp, _vp, _vp, _sz, _vp]),
+    "litevlm_select_score_topk": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _f32,
+                                         _f32, _vp, _vp, _vp, _f32, _f32, _f32, _f32, _f64, _vp, _vp, _vp,
+                                         _vp, _vp, _vp, _vp, _vp, _vp, _vp, _sz, _vp]),
     "litevlm_prefill_attn": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _i32,
                                     _f32, _f32, _f32, _f32, _i32, _vp, _vp]),
     "litevlm_tsm_qk": (_i32, [_i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp, _vp, _vp, _f32, _f32,

@@ -138,7 +138,9 @@ litevlm_status_t launch_score(int32_t dtype, int32_t B, int32_t S, int32_t V_ful
                               int32_t D, int32_t query_rows, const void* q, const void* k, const void* v,
                               float softmax_scale, float q_scale, float k_scale, const uint8_t* token_keep,
                               double keep_ratio, float* scores, int32_t* kept_index, int32_t* cu_seqlens,
-                              void* qc, void* kc, void* vc, void* workspace, void* stream) {
+                              void* qc, void* kc, void* vc, void* workspace, void* stream,
+                              const ViewSel* vs = nullptr, uint8_t* view_keep = nullptr,
+                              uint8_t* token_keep_out = nullptr, int32_t* n_visual_kept = nullptr) {
   ScoreArgs a;
   a.dtype = dtype;
   a.B = B;
@@ -161,6 +163,12 @@ litevlm_status_t launch_score(int32_t dtype, int32_t B, int32_t S, int32_t V_ful
   a.kc = kc;
   a.vc = vc;
   a.workspace = workspace;
+  if (vs) {
+    a.vs = *vs;
+    a.view_keep = view_keep;
+    a.token_keep_out = token_keep_out;
+    a.n_visual_kept = n_visual_kept;
+  }
   return hip_status(launch_token_score_topk(a, static_cast<hipStream_t>(stream)));
 }
 
@@ -236,6 +244,46 @@ litevlm_status_t litevlm_token_score_topk_rows(int32_t dtype, int32_t B, int32_t
   if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
   return launch_score(dtype, B, S, V_full, Hq, Hkv, D, query_rows, q, k, v, softmax_scale, q_scale, k_scale,
                       token_keep, keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc, workspace, stream);
+}
+
+litevlm_status_t litevlm_select_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full, int32_t Hq,
+                                           int32_t Hkv, int32_t D, int32_t N, const int32_t* view_offsets_host,
+                                           const float* view_logit, const float* view_lexical, float w_lexical,
+                                           float threshold, const void* q, const void* k, const void* v,
+                                           float softmax_scale, float q_scale, float k_scale, float v_scale,
+                                           double keep_ratio, uint8_t* view_keep, uint8_t* token_keep,
+                                           int32_t* n_visual_kept, float* scores, int32_t* kept_index,
+                                           int32_t* cu_seqlens, void* qc, void* kc, void* vc, void* workspace,
+                                           size_t workspace_bytes, void* stream) {
+  const int32_t T = S > V_full ? S - V_full : 1;
+  const litevlm_status_t st =
+      check_score_args(dtype, B, S, V_full, Hq, Hkv, D, T, q, k, v, softmax_scale, q_scale, k_scale, v_scale,
+                       keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc);
+  if (st != LITEVLM_OK) return st;
+  if (!view_offsets_host || !view_logit) return LITEVLM_ERR_NULL_POINTER;
+  if (N < 1 || N > LITEVLM_MAX_VIEWS || view_offsets_host[0] != 0) return LITEVLM_ERR_BAD_SHAPE;
+  if (N > kFusedViews) return LITEVLM_ERR_UNSUPPORTED;
+  ViewSel vs{};
+  for (int v = 0; v <= N; ++v) {
+    vs.off[v] = view_offsets_host[v];
+    if (v > 0 && vs.off[v] < vs.off[v - 1]) return LITEVLM_ERR_BAD_SHAPE;
+  }
+  if (vs.off[N] != V_full) return LITEVLM_ERR_BAD_SHAPE;  // the views tile the visual positions
+  if (!(w_lexical >= 0.f && w_lexical <= 1.f) || !isfinite(threshold)) return LITEVLM_ERR_BAD_VALUE;
+  if (!aligned(view_logit, 4) || (view_lexical && !aligned(view_lexical, 4)) ||
+      (n_visual_kept && !aligned(n_visual_kept, 4)))
+    return LITEVLM_ERR_MISALIGNED;
+  if (workspace && !aligned(workspace, 16)) return LITEVLM_ERR_MISALIGNED;
+  const size_t need = score_workspace_layout(B, S, V_full, Hq, Hkv, T).total;
+  if (!workspace || workspace_bytes < need) return LITEVLM_ERR_WORKSPACE;
+  vs.logit = view_logit;
+  vs.lexical = view_lexical;
+  vs.w = w_lexical;
+  vs.tau = threshold;
+  vs.N = N;
+  return launch_score(dtype, B, S, V_full, Hq, Hkv, D, T, q, k, v, softmax_scale, q_scale, k_scale, nullptr,
+                      keep_ratio, scores, kept_index, cu_seqlens, qc, kc, vc, workspace, stream, &vs, view_keep,
+                      token_keep, n_visual_kept);
 }
 
 litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, int32_t V_full,

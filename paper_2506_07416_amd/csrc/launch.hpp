@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "../../include/litevlm.h"
+#include "viewsel.hpp"
 
 namespace litevlm {
 
@@ -44,6 +45,12 @@ struct ScoreArgs {
   void* kc;
   void* vc;
   void* workspace;
+  // in-call patch selection (vs.N > 0, token_keep NULL): the keep flags come
+  // from the view scores, and the selection's outputs are written (each may be NULL)
+  ViewSel vs{};
+  uint8_t* view_keep = nullptr;
+  uint8_t* token_keep_out = nullptr;
+  int32_t* n_visual_kept = nullptr;
 };
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream);
 

@@ -3,6 +3,7 @@
 // token mask over the view-major visual layout plus the always-kept text.
 #include "common.hpp"
 #include "launch.hpp"
+#include "viewsel.hpp"
 
 namespace litevlm {
 
@@ -11,39 +12,21 @@ patch_select_kernel(int N, int S, ViewOffsets vo, const float* __restrict__ logi
                     const float* __restrict__ lexical, float w, float tau,
                     uint8_t* __restrict__ view_keep, uint8_t* __restrict__ token_keep,
                     int32_t* __restrict__ n_visual_kept) {
-  const int b = blockIdx.x, tid = threadIdx.x;
-  __shared__ uint8_t keep_s[LITEVLM_MAX_VIEWS];
-  __shared__ float s_s[LITEVLM_MAX_VIEWS];
+  const int b = blockIdx.x, tid = threadIdx.x, lane = tid & 63;
   __shared__ int off_s[LITEVLM_MAX_VIEWS + 1];
   // the view offsets go to LDS once, so that no loop below waits on a
   // dependent load of them
   if (tid <= N) off_s[tid] = vo.off[tid];
-  // One thread per view, written as the definition reads: no FMA
-  // contraction and IEEE division, so the decision matches an fp32 evaluation.
-  if (tid < N) {
-    const float x = logit[b * N + tid];
-    const float sig = __fdiv_rn(1.0f, __fadd_rn(1.0f, expf(-x)));
-    const float lex = lexical ? lexical[b * N + tid] : 0.0f;
-    const float s = __fadd_rn(__fmul_rn(w, lex), __fmul_rn(__fsub_rn(1.0f, w), sig));
-    s_s[tid] = s;
-    keep_s[tid] = (uint8_t)(s > tau);
-  }
+  // every wave takes the decision, one view per lane (N <= 64), with the
+  // function the scoring kernels use when they select the views themselves
+  const ViewIn in = view_load(logit, lexical, N, b, lane);
+  const uint64_t mask = view_keep_mask<LITEVLM_MAX_VIEWS>(in, lexical != nullptr, w, tau, N, lane);
   __syncthreads();
-  if (tid == 0) {
-    // if no view passes, keep the best one (lowest index among equal scores)
-    int any = 0, best_v = 0;
-    for (int v = 0; v < N; ++v) {
-      any |= keep_s[v];
-      if (s_s[v] > s_s[best_v]) best_v = v;
-    }
-    if (!any) keep_s[best_v] = 1;
-  }
-  __syncthreads();
-  if (tid < N) view_keep[b * N + tid] = keep_s[tid];
+  if (tid < N) view_keep[b * N + tid] = (uint8_t)((mask >> tid) & 1u);
   if (tid == 0 && n_visual_kept) {
     int nvis = 0;
     for (int v = 0; v < N; ++v)
-      if (keep_s[v]) nvis += off_s[v + 1] - off_s[v];
+      if ((mask >> v) & 1u) nvis += off_s[v + 1] - off_s[v];
     n_visual_kept[b] = nvis;
   }
   // token mask: visual token p takes its view's flag (views are contiguous
@@ -59,14 +42,14 @@ patch_select_kernel(int N, int S, ViewOffsets vo, const float* __restrict__ logi
     uint32_t wd[4];
     if (p0 + n <= (v < N ? off_s[v + 1] : S)) {
       // the whole chunk lies in one view (or in the text)
-      const uint32_t k = v < N ? keep_s[v] : 1u;
+      const uint32_t k = v < N ? (uint32_t)((mask >> v) & 1u) : 1u;
       wd[0] = wd[1] = wd[2] = wd[3] = k * 0x01010101u;
     } else {
       wd[0] = wd[1] = wd[2] = wd[3] = 0u;
       for (int j = 0; j < n; ++j) {
         const int p = p0 + j;
         while (v < N && p >= off_s[v + 1]) ++v;
-        const uint32_t k = v < N ? keep_s[v] : 1u;
+        const uint32_t k = v < N ? (uint32_t)((mask >> v) & 1u) : 1u;
         wd[j >> 2] |= k << (8 * (j & 3));
       }
     }

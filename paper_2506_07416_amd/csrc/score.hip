@@ -24,6 +24,7 @@
 
 #include "common.hpp"
 #include "launch.hpp"
+#include "viewsel.hpp"
 
 namespace litevlm {
 
@@ -42,6 +43,11 @@ constexpr int CH = 32;                      // query rows per chunk
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Column sum of a visual key of a dropped view when the scoring takes the view
+// selection itself: sweep 2 stores it (no sum reaches 2^62), so that the top-k
+// reads the keep flags with the sums instead of evaluating the selection per key.
+constexpr unsigned long long kDroppedCol = ~0ull;
+
 // Work split of the sweeps (a function of the shape only, so that the
 // workspace size is too).
 struct ScoreSplit {
@@ -55,6 +61,9 @@ struct ScoreDims {
   int n_rb, n_kt, ns1, n_vt, nchunks, rs2;
   float scale_log2;
   float fx;  // fixed-point scale of the column sums (a power of two)
+  // in-call patch selection (the kernels' VSEL instances): keep flags from the
+  // view scores instead of a token mask
+  ViewSel vs;
 };
 
 template <int N>
@@ -401,7 +410,7 @@ __device__ __forceinline__ int keys_upto(int L) {
 // not computed. Output: rowpart[b][g][split][row] = (max, sum), max in log2
 // units.
 
-template <int DT, int D>
+template <int DT, int D, bool VSEL>
 __global__ void __launch_bounds__(kSweepThreads)
 score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                       const uint8_t* __restrict__ token_keep, float2* __restrict__ rowpart,
@@ -481,7 +490,9 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   if (Tile::QSTAGE) q_round(0);
   asm volatile("" ::: "memory");  // keep the copies ahead of the keep-byte loads
   uint8_t kf[kFlagsPer];
-  load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
+  ViewIn vin;
+  if constexpr (VSEL) vin = view_load(d.vs.logit, d.vs.lexical, d.vs.N, b, lane);
+  else load_keep_bytes(keep_row, tile0, d.V_full, w, lane, kf);
   if (Tile::QSTAGE) {
     wait_vmcnt<0>();  // round 0, the first key tiles and the keep bytes have landed
     __syncthreads();
@@ -499,6 +510,15 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   }
   pipe.wait_for(0);
   __syncthreads();  // tile 0 and the keep bytes have landed
+  if constexpr (VSEL) {
+    // the keep flags of the lane's keys from the sample's view selection
+    const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(vin, d.vs.lexical != nullptr, d.vs.w, d.vs.tau, d.vs.N, lane);
+#pragma unroll
+    for (int i = 0; i < kFlagsPer; ++i) {
+      const int key = (tile0 + w + kSweepWaves * i) * KB + lane;
+      kf[i] = d.V_full > 0 ? (uint8_t)view_token_flag(d.vs, vm, min(key, d.V_full - 1)) : 1;
+    }
+  }
   uint64_t live, plain;
   tile_flags(mw, keepl, kf, tile0, ntl, d.V_full, d.S, w, lane, live, plain);
 
@@ -831,7 +851,7 @@ __device__ __forceinline__ bool block_any(bool v, uint32_t* slots) {
 
 constexpr int kMaxChunksPerSplit = 32;  // row chunks of one sweep-2 workgroup (table of 8 KB)
 
-template <int DT, int D>
+template <int DT, int D, bool VSEL>
 __global__ void __launch_bounds__(256, DT == LITEVLM_F32 ? 2 : 3)  // fp32 chunks: 16 KB each
 score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __restrict__ kv,
                      const uint8_t* __restrict__ token_keep, const float2* __restrict__ rowpart,
@@ -886,7 +906,10 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   // an unconditional load (of a valid byte when there is no mask), so that no
   // branch makes the compiler wait for every load in flight here
   const uint8_t* tkp = keep_row ? keep_row + min(tkey, d.V_full - 1) : static_cast<const uint8_t*>(kv);
-  const uint8_t tkraw = *tkp;
+  uint8_t tkraw = 1;
+  ViewIn vin;
+  if constexpr (VSEL) vin = view_load(d.vs.logit, d.vs.lexical, d.vs.N, b, lane);
+  else tkraw = *tkp;
   Ring ring;
   ring.init(q, b, g, d, w, lane, row0, cstep);
   Tile tile;
@@ -949,8 +972,13 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
       lds_store_f2(table + lr, e);
     }
   }
-  const uint8_t tkb = keep_row ? tkraw : 1;
+  uint32_t vm = 0;
+  if constexpr (VSEL) vm = (uint32_t)view_keep_mask<kFusedViews>(vin, d.vs.lexical != nullptr, d.vs.w, d.vs.tau, d.vs.N, lane);
+  const uint8_t tkb = VSEL ? (uint8_t)view_token_flag(d.vs, vm, min(tkey, d.V_full - 1)) : (keep_row ? tkraw : 1);
   const bool tkept = tkey < d.V_full && tkb != 0;
+  // the mark of a dropped key's column, from one workgroup per key tile (no
+  // other workgroup writes a dropped key's column)
+  if (VSEL && g == 0 && rs == 0 && tkey < d.V_full && tkb == 0) acc[(size_t)b * d.V_full + tkey] = kDroppedCol;
   if (!block_any(tkept, reinterpret_cast<uint32_t*>(lds + FLG))) {
     // no kept key in the tile: nothing to add (the copies into LDS land
     // before the workgroup ends)
@@ -1006,7 +1034,7 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
   const float colmass = (hl ? tot[1] : tot[0]) + got;
   const int key = key0 + lane;
   // dropped keys were summed over too; their column stays 0
-  if (key < d.V_full && (keep_row == nullptr || keep_row[key]))
+  if (key < d.V_full && (VSEL ? view_token_flag(d.vs, vm, key) != 0 : (keep_row == nullptr || keep_row[key])))
     __hip_atomic_fetch_add(acc + (size_t)b * d.V_full + key, (unsigned long long)__float2ll_rn(colmass * d.fx),
                            __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -1096,10 +1124,16 @@ __device__ __forceinline__ int block_scan_excl(int v, int* wsum, int* total) {
 // over the Hq*T text rows; -inf for dropped tokens), their order keys, radix
 // select of the k_b-th largest key (12-bit digits below the common prefix of
 // the kept keys), then the stable compaction.
+// VSEL: the keep flags come from the view selection (vs), and the selection's
+// outputs are written here: view_keep [B, N], the token mask [B, S] and the
+// kept-visual counts [B] (each may be NULL).
+template <bool VSEL>
 __global__ void __launch_bounds__(kTopkThreads)
 topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restrict__ token_keep,
                     const unsigned long long* __restrict__ acc, double inv, float* __restrict__ scores,
-                    int32_t* __restrict__ kept_index, int32_t* __restrict__ cu_seqlens) {
+                    int32_t* __restrict__ kept_index, int32_t* __restrict__ cu_seqlens, ViewSel vs,
+                    uint8_t* __restrict__ view_keep_out, uint8_t* __restrict__ token_keep_out,
+                    int32_t* __restrict__ n_visual_out) {
   __shared__ uint32_t keys[LITEVLM_MAX_VISUAL];
   __shared__ int hist[kBins];
   __shared__ int vcnt[LITEVLM_MAX_BATCH];
@@ -1116,6 +1150,9 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   // thread's rounds are all in flight at once, together with the loads of the
   // kept-visual counts below.
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * S : nullptr;
+  // the sample's view selection, requested first (its mask gives every keep flag)
+  ViewIn vin;
+  if constexpr (VSEL) vin = view_load(vs.logit, vs.lexical, vs.N, b, lane);
   const unsigned long long* ac = acc + (size_t)b * V_full;
   float* sc = scores + (size_t)b * V_full;
   auto score_of = [&](unsigned long long v, bool kept) { return kept ? (float)((double)v * inv) : -INFINITY; };
@@ -1133,17 +1170,53 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
       const int j4 = min(4 * (tid + i * kTopkThreads), V_full - 4);
       a4[i][0] = *reinterpret_cast<const u64x2*>(ac + j4);
       a4[i][1] = *reinterpret_cast<const u64x2*>(ac + j4 + 2);
-      // unconditional load (of valid bytes when there is no mask): no branch
-      const uint32_t* fp = keep_row ? reinterpret_cast<const uint32_t*>(keep_row + j4)
-                                    : reinterpret_cast<const uint32_t*>(ac + j4);
-      const uint32_t fraw = *fp;
-      f4[i] = keep_row ? fraw : 0x01010101u;
+      if constexpr (!VSEL) {
+        // unconditional load (of valid bytes when there is no mask): no branch
+        const uint32_t* fp = keep_row ? reinterpret_cast<const uint32_t*>(keep_row + j4)
+                                      : reinterpret_cast<const uint32_t*>(ac + j4);
+        const uint32_t fraw = *fp;
+        f4[i] = keep_row ? fraw : 0x01010101u;
+      }
     }
+  }
+  if constexpr (VSEL) {
+    // keep flags from the column sums (dropped keys carry kDroppedCol), and
+    // the selection's outputs for this sample
+    const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(vin, vs.lexical != nullptr, vs.w, vs.tau, vs.N, lane);
+    if (view_keep_out && tid < vs.N) view_keep_out[(size_t)b * vs.N + tid] = (uint8_t)((vm >> tid) & 1u);
+    uint8_t* row = token_keep_out ? token_keep_out + (size_t)b * S : nullptr;
+    if (vec) {
+#pragma unroll
+      for (int i = 0; i < R4; ++i) {
+        const unsigned long long av[4] = {a4[i][0].x, a4[i][0].y, a4[i][1].x, a4[i][1].y};
+        uint32_t f = 0;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) f |= (uint32_t)(av[u] != kDroppedCol) << (8 * u);
+        f4[i] = f;
+        const int j4 = 4 * (tid + i * kTopkThreads);
+        if (row && j4 < V_full) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) row[j4 + u] = (uint8_t)((f >> (8 * u)) & 1u);
+        }
+      }
+    } else if (row) {
+      for (int j = tid; j < V_full; j += kTopkThreads) row[j] = (uint8_t)(ac[j] != kDroppedCol);
+    }
+    if (row)
+      for (int j = V_full + tid; j < S; j += kTopkThreads) row[j] = 1;
   }
 
   // Kept-visual counts of samples 0..b, one sample per wave at a time.
   for (int bb = wave; bb <= b; bb += kTopkWaves) {
-    const int c = token_keep ? wave_count_flags(token_keep + (size_t)bb * S, V_full, lane) : V_full;
+    int c;
+    if constexpr (VSEL) {
+      const uint32_t m = (uint32_t)view_keep_mask<kFusedViews>(view_load(vs.logit, vs.lexical, vs.N, bb, lane),
+                                                  vs.lexical != nullptr, vs.w, vs.tau, vs.N, lane);
+      c = 0;
+      for (int v = 0; v < vs.N; ++v) c += ((m >> v) & 1u) ? vs.off[v + 1] - vs.off[v] : 0;
+    } else {
+      c = token_keep ? wave_count_flags(token_keep + (size_t)bb * S, V_full, lane) : V_full;
+    }
     if (lane == 0) vcnt[bb] = c;
   }
   for (int i = tid; i < kBins; i += kTopkThreads) hist[i] = 0;
@@ -1171,7 +1244,7 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
     }
   } else {
     for (int j = tid; j < V_full; j += kTopkThreads) {
-      const bool kept = keep_row == nullptr || keep_row[j];
+      const bool kept = VSEL ? ac[j] != kDroppedCol : (keep_row == nullptr || keep_row[j]);
       const float sv = score_of(ac[j], kept);
       sc[j] = sv;
       const uint32_t key = kept ? order_key(sv) : 0u;
@@ -1211,6 +1284,7 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
     for (int w = 0; w < kTopkWaves; ++w) cu_b += wsum[0][w];
   }
   const int kb_ = keep_count(keep_ratio, vcnt[b]);
+  if (VSEL && n_visual_out && tid == 0) n_visual_out[b] = vcnt[b];
 
   // Radix select of the kb_-th largest key. Bits above the highest bit where
   // kmin and kmax differ are common to every kept key and are skipped.
@@ -1426,14 +1500,23 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv,
 // Flat XCD-aware grids: 8 XCDs x (columns per XCD, rounded up) x splits.
 static int sweep_grid(long long ncol, int nsplit) { return (int)(8 * ((ncol + 7) / 8) * nsplit); }
 
+template <int DT, int D, bool VSEL>
+static void launch_sweeps_v(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp, float2* rowpart,
+                            unsigned long long* acc, hipStream_t stream) {
+  hipLaunchKernelGGL((score_rowstats_kernel<DT, D, VSEL>),
+                     dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_rb, sp.ns1)), dim3(kSweepThreads), 0, stream, d,
+                     a.q, a.k, a.token_keep, rowpart, acc);
+  if (sp.n_vt > 0)
+    hipLaunchKernelGGL((score_colmass_kernel<DT, D, VSEL>),
+                       dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_vt, sp.rs2)), dim3(64 * kColWaves), 0, stream,
+                       d, a.q, a.k, a.token_keep, rowpart, acc);
+}
+
 template <int DT, int D>
 static void launch_sweeps(const ScoreArgs& a, const ScoreDims& d, const ScoreSplit& sp, float2* rowpart,
                           unsigned long long* acc, hipStream_t stream) {
-  hipLaunchKernelGGL((score_rowstats_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_rb, sp.ns1)),
-                     dim3(kSweepThreads), 0, stream, d, a.q, a.k, a.token_keep, rowpart, acc);
-  if (sp.n_vt > 0)
-    hipLaunchKernelGGL((score_colmass_kernel<DT, D>), dim3(sweep_grid((long long)a.B * a.Hkv * sp.n_vt, sp.rs2)),
-                       dim3(64 * kColWaves), 0, stream, d, a.q, a.k, a.token_keep, rowpart, acc);
+  if (d.vs.N > 0) launch_sweeps_v<DT, D, true>(a, d, sp, rowpart, acc, stream);
+  else launch_sweeps_v<DT, D, false>(a, d, sp, rowpart, acc, stream);
 }
 
 hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
@@ -1459,6 +1542,7 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.nchunks = sp.nchunks;
   d.rs2 = sp.rs2;
   d.scale_log2 = a.logit_scale_log2;
+  d.vs = a.vs;
   // A text row adds at most 1 to a column, so a column sum is at most Hq*T:
   // with Hq*T <= 2^e, fx = 2^(62-e) keeps every sum below 2^62.
   const double rows = (double)a.Hq * (double)d.T;
@@ -1475,8 +1559,14 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   else LITEVLM_SWEEPS(LITEVLM_F32);
 #undef LITEVLM_SWEEPS
 
-  hipLaunchKernelGGL(topk_compact_kernel, dim3(a.B), dim3(kTopkThreads), 0, stream, a.S, a.V_full,
-                     a.keep_ratio, a.token_keep, acc, inv, a.scores, a.kept_index, a.cu_seqlens);
+  if (a.vs.N > 0)
+    hipLaunchKernelGGL(topk_compact_kernel<true>, dim3(a.B), dim3(kTopkThreads), 0, stream, a.S, a.V_full,
+                       a.keep_ratio, a.token_keep, acc, inv, a.scores, a.kept_index, a.cu_seqlens, a.vs,
+                       a.view_keep, a.token_keep_out, a.n_visual_kept);
+  else
+    hipLaunchKernelGGL(topk_compact_kernel<false>, dim3(a.B), dim3(kTopkThreads), 0, stream, a.S, a.V_full,
+                       a.keep_ratio, a.token_keep, acc, inv, a.scores, a.kept_index, a.cu_seqlens, a.vs,
+                       nullptr, nullptr, nullptr);
   if (a.qc || a.kc || a.vc) {
     const int esz = a.dtype == LITEVLM_F32 ? 4 : (a.dtype == LITEVLM_BF16 ? 2 : 1);
     launch_gather(a.B, a.S, a.kept_index, a.cu_seqlens, a.q, a.k, a.v, a.qc, a.kc, a.vc,

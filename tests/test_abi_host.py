@@ -44,6 +44,7 @@ def test_header_constants_match_binding():
     assert int(re.search(r"LITEVLM_MAX_VISUAL (\d+)", text).group(1)) == _abi.MAX_VISUAL
     assert int(re.search(r"LITEVLM_MAX_BATCH (\d+)", text).group(1)) == _abi.MAX_BATCH
     assert int(re.search(r"LITEVLM_MAX_HEADS (\d+)", text).group(1)) == _abi.MAX_HEADS
+    assert int(re.search(r"LITEVLM_MAX_FUSED_VIEWS (\d+)", text).group(1)) == _abi.MAX_FUSED_VIEWS
 
 
 # ----------------------------------------------------------------------------- patch_select
@@ -69,6 +70,39 @@ def test_patch_select_validation():
     assert ps(tau=float("inf")) == _abi.ERR_BAD_VALUE
     assert ps(logit=A + 2) == _abi.ERR_MISALIGNED
     assert ps(nv=A + 1) == _abi.ERR_MISALIGNED
+
+
+# ----------------------------------------------------------------------------- select_score_topk
+
+def sst(N=3, off=(0, 20, 40, 80), logit=A, lex=None, w=0.0, tau=0.5, B=1, S=100, V=80, ws=A, wsb=None,
+        q=A, vk=A, tk=A, nv=A):
+    lib = lv.load()
+    if wsb is None:
+        wsb = lib.litevlm_token_score_topk_workspace(B, S, V, 8, 2, 128)
+    offs = None if off is None else (ctypes.c_int32 * len(off))(*off)
+    return lib.litevlm_select_score_topk(_abi.BF16, B, S, V, 8, 2, 128, N, offs, logit, lex, w, tau, q, A, A,
+                                         0.088, 1.0, 1.0, 1.0, 0.5, vk, tk, nv, A, A, A, A, A, A, ws, wsb,
+                                         None)
+
+
+def test_select_score_topk_validation():
+    assert sst(logit=None) == _abi.ERR_NULL_POINTER
+    assert sst(off=None) == _abi.ERR_NULL_POINTER
+    assert sst(q=None) == _abi.ERR_NULL_POINTER
+    assert sst(N=0) == _abi.ERR_BAD_SHAPE
+    assert sst(off=(1, 20, 40, 80)) == _abi.ERR_BAD_SHAPE       # must start at 0
+    assert sst(off=(0, 40, 20, 80)) == _abi.ERR_BAD_SHAPE       # must ascend
+    assert sst(off=(0, 20, 40, 70)) == _abi.ERR_BAD_SHAPE       # the views must end at V_full
+    assert sst(N=9, off=tuple(range(0, 81, 10))) == _abi.ERR_UNSUPPORTED   # beyond the fused limit
+    assert sst(N=65, off=tuple(range(66))) == _abi.ERR_BAD_SHAPE
+    assert sst(w=1.5) == _abi.ERR_BAD_VALUE
+    assert sst(tau=float("nan")) == _abi.ERR_BAD_VALUE
+    assert sst(logit=A + 2) == _abi.ERR_MISALIGNED
+    assert sst(nv=A + 1) == _abi.ERR_MISALIGNED
+    assert sst(ws=None) == _abi.ERR_WORKSPACE
+    assert sst(wsb=16) == _abi.ERR_WORKSPACE
+    # the selection outputs are optional
+    assert sst(vk=None, tk=None, nv=None, ws=None) == _abi.ERR_WORKSPACE
 
 
 # ----------------------------------------------------------------------------- token_score_topk

@@ -231,6 +231,90 @@ def test_select_chain_matches_oracle(name):
     log(f"  attention {stats}")
 
 
+# ----------------------------------------------------------------------------- in-call patch selection
+
+def run_fused(case, keep_ratio=None, logit=None, lexical=None, w=None, tau=None):
+    """litevlm_select_score_topk on the GPU; host copies in run_select's layout."""
+    r = case.keep_ratio if keep_ratio is None else keep_ratio
+    q, k, v = (to_device(x, case.dtype) for x in (case.q, case.k, case.v))
+    lg = torch.from_numpy(case.view_logit if logit is None else logit).cuda()
+    lx = None if lexical is None else torch.from_numpy(lexical).cuda()
+    out = lv.select_score_topk(lg, case.view_offsets, q, k, v, r, case.V_full,
+                               w_lexical=case.w_lexical if w is None else w,
+                               threshold=case.threshold if tau is None else tau, view_lexical=lx,
+                               q_scale=case.q_scale, k_scale=case.k_scale, v_scale=case.v_scale)
+    torch.cuda.synchronize()
+    cu = out["cu_seqlens"].cpu().numpy()
+    return dict(view_keep=out["view_keep"].cpu().numpy(), token_keep=out["token_keep"].cpu().numpy(),
+                n_vis=out["n_visual_kept"].cpu().numpy(), scores=out["scores"].cpu().numpy().astype(np.float64),
+                cu=cu, kept_index=out["kept_index"][:cu[-1]].cpu().numpy(), dev=out)
+
+
+def run_two_calls(case, keep_ratio, logit, lexical, w, tau):
+    """patch_select then token_score_topk with explicit selection inputs."""
+    q, k, v = (to_device(x, case.dtype) for x in (case.q, case.k, case.v))
+    vk, tk, nv = lv.patch_select(torch.from_numpy(logit).cuda(), case.view_offsets, case.S, w, tau,
+                                 view_lexical=None if lexical is None else torch.from_numpy(lexical).cuda())
+    out = lv.token_score_topk(q, k, v, tk, keep_ratio, case.V_full, q_scale=case.q_scale,
+                              k_scale=case.k_scale, v_scale=case.v_scale)
+    torch.cuda.synchronize()
+    cu = out["cu_seqlens"].cpu().numpy()
+    return dict(view_keep=vk.cpu().numpy(), token_keep=tk.cpu().numpy(), n_vis=nv.cpu().numpy(),
+                scores=out["scores"].cpu().numpy().astype(np.float64), cu=cu,
+                kept_index=out["kept_index"][:cu[-1]].cpu().numpy(), dev=out)
+
+
+def assert_same_select(a, b, label):
+    """Every output of two selection runs bit for bit (the packed rows up to cu[B])."""
+    for key in ("view_keep", "token_keep", "n_vis", "cu", "kept_index"):
+        assert np.array_equal(a[key], b[key]), f"{label}: {key}"
+    assert np.array_equal(a["scores"].astype(np.float32).view(np.uint32),
+                          b["scores"].astype(np.float32).view(np.uint32)), f"{label}: scores"
+    rows = int(a["cu"][-1])
+    for name in ("qc", "kc", "vc"):
+        assert torch.equal(bits_of_t(a["dev"][name][:rows]), bits_of_t(b["dev"][name][:rows])), f"{label}: {name}"
+
+
+def bits_of_t(t):
+    return t.contiguous().view(torch.uint8)
+
+
+@pytest.mark.parametrize("cfg,r", [(2, None), (3, 0.5), (3, 0.25), (4, None), (5, None), (1, None)])
+def test_fused_select_equals_two_calls(cfg, r):
+    """The in-call selection gives the two-call path's results bit for bit, at
+    the workload shapes (cfg3-5 full size, cfg4 with masked views, fp8, fp32),
+    and the oracle's selection."""
+    case = synth.config_case(cfg)
+    r = case.keep_ratio if r is None else r
+    log(f"fused select cfg{cfg}: B={case.B} S={case.S} N={case.N} {case.dtype} r={r}")
+    g = run_fused(case, keep_ratio=r)
+    two = run_two_calls(case, r, case.view_logit, None, case.w_lexical, case.threshold)
+    assert_same_select(g, two, f"cfg{cfg}")
+    if cfg in (1, 2):
+        check_select(case, g, oracle.run_path(case, keep_ratio=r, attention=False), f"fused cfg{cfg}")
+
+
+def test_fused_select_random_logits_lexical_fallback():
+    """Logits near the threshold, lexical scores, and samples where no view
+    passes (the best-view fallback): the in-call decision is the patch-select
+    kernel's, bit for bit, for several (w, tau)."""
+    rng = np.random.default_rng(21)
+    case = synth.config_case(2, B=12, N=6, Tv=40, T=16, Hq=8, Hkv=2, D=128)
+    tau0 = 0.6
+    x0 = math.log(tau0 / (1 - tau0))
+    logit = (x0 + rng.normal(0, 1e-3, (case.B, case.N))).astype(np.float32)
+    logit[2] = -15.0
+    logit[5, :] = x0 - 1.0
+    lex = rng.random((case.B, case.N)).astype(np.float32)
+    for w, tau, lx in ((0.0, tau0, None), (0.3, 0.55, lex), (1.0, 0.7, lex), (0.0, 0.999, None)):
+        g = run_fused(case, logit=logit, lexical=lx, w=w, tau=tau)
+        two = run_two_calls(case, case.keep_ratio, logit, lx, w, tau)
+        assert_same_select(g, two, f"w={w} tau={tau}")
+        n_band = check_view_keep(oracle.view_scores(logit, lx, w), tau, g["view_keep"])
+        log(f"fused w={w} tau={tau}: views kept {int(g['view_keep'].sum())} of {case.B * case.N}, "
+            f"{n_band} in the threshold band")
+
+
 # scoring from the last n text tokens only (n = 1: the last-token readout)
 ROWS_CASES = [
     ("rows1-cfg2", dict(cfg=2), 1),
