@@ -85,8 +85,14 @@ def gather_bytes(seqlens, Hq, Hkv, D, e):
 
 
 def source_hash(path):
-    with open(path, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of a kernel source together with the device headers it includes
+    (every .hpp beside it), so that a change to either voids old counters."""
+    h = hashlib.sha256()
+    d = os.path.dirname(path)
+    for p in [path] + sorted(os.path.join(d, f) for f in os.listdir(d) if f.endswith(".hpp")):
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def kernel_base(name):
