@@ -29,6 +29,7 @@ struct AttnParams {
   const int32_t* cu;
   void* o;
   int B, Hq, Hkv, G, n_mtiles, n_work, per_xcd;
+  int Hw, P;  // pipelined bf16 path: query heads per workgroup, 32-position blocks per workgroup
   float scale_log2, out_scale;
 };
 
@@ -361,6 +362,365 @@ attn_bf16_kernel(AttnParams p) {
 }
 
 // ---------------------------------------------------------------------------
+// bf16 path for grids that fit one pass of the chip (at most two workgroups
+// per CU): a software-pipelined tile loop, for when one workgroup's chain of
+// key tiles is the critical path rather than the chip's throughput.
+//
+// A workgroup is 4 waves and covers 128 (query position, head) rows of one KV
+// head: Hw query heads (the largest of 4, 2, 1 dividing G) times 32*(4/Hw)
+// consecutive positions. Wave w takes head w % Hw and the 32 positions of
+// block w / Hw; at the GQA shapes (G = 4) the four waves are the four query
+// heads of one 32-position block, so they share one causal extent and every
+// K/V tile is staged once for all of them.
+//
+// K and V tiles of 64 keys are copied global -> LDS directly into rings of two
+// slots each, one tile ahead of use. A wave keeps its 32 query rows in
+// registers and computes, per key tile t:
+//   (a) the mask (edge tiles only) and the row max of S_t = K_t Q^T, formed in
+//       the previous step; the output is rescaled only when a row's max grows
+//       by more than 2^8 (so every p <= 2^8);
+//   (b) the exponentials P_t = exp2(S_t*c - m*c), packed to bf16 as they are
+//       formed and issued between the MFMAs of S_{t+1} = K_{t+1} Q^T, so the
+//       matrix pipe runs the next tile's logits under this tile's vector work
+//       (the last tile also forms the logits of a stale slot, discarded, so the
+//       loop needs no separate tail);
+//   (c) O^T += V_t^T P_t^T, the transposed V reads two 16-key steps ahead.
+// One barrier per tile hands the ring slots over. About 240 VGPRs: two waves
+// per SIMD.
+
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+// Workgroup barrier with only the LDS wait spelled out (the copies in flight
+// are waited for explicitly by the caller; the fence of __syncthreads would
+// wait for all of them). The memory clobber keeps LDS accesses on their side.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Transposed LDS read (ds_read_b64_tr_b16) as inline assembly: the builtin
+// makes the compiler wait for every direct copy in flight before it, which
+// would drain the copies issued ahead. The caller waits (lgkmcnt) before use.
+template <int OFF>
+__device__ __forceinline__ s16x4 ds_read_tr16(uint32_t addr) {
+  s16x4 r;
+  asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(r) : "v"(addr), "i"(OFF));
+  return r;
+}
+
+// The V operands of one key tile: va[kk][db] = V^T rows 32*db.., keys 16*kk..
+// (two transposed reads of 4 keys each per lane, rows 4 apart).
+template <int RB, int DB, int KK>
+__device__ __forceinline__ void vread_kk(bf16x8 (&va)[DB], const uint32_t (&vaddr)[DB]) {
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const s16x4 lo = ds_read_tr16<(16 * KK) * RB>(vaddr[db]);
+    const s16x4 hi = ds_read_tr16<(16 * KK + 4) * RB>(vaddr[db]);
+    va[db] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
+}
+
+// Wait until at most N LDS accesses of the wave remain; the operands pass
+// through the wait, so that nothing reading them is placed before it.
+template <int N, int DB>
+__device__ __forceinline__ void lds_wait_n(bf16x8 (&a)[DB]) {
+  if constexpr (DB == 4)
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a[0]), "+v"(a[1]), "+v"(a[2]), "+v"(a[3]) : "i"(N));
+  else
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(a[0]), "+v"(a[1]) : "i"(N));
+}
+
+// Work item (KV head g, head group hgrp of Hw heads, query block mt from the
+// last, sample b), dealt to the 8 XCDs in contiguous ranges: an XCD owns whole
+// KV heads across the batch, so workgroups sharing K/V sit behind the same L2,
+// and within an XCD the longest causal blocks start first.
+__device__ __forceinline__ bool decode_work_hg(const AttnParams& p, int& b, int& g, int& hgrp, int& mt) {
+  const int L = blockIdx.x;
+  const int w = (L & 7) * p.per_xcd + (L >> 3);
+  if (w >= p.n_work) return false;
+  const int ng = p.G / p.Hw;
+  b = w % p.B;
+  int rest = w / p.B;
+  const int mrev = rest % p.n_mtiles;
+  rest /= p.n_mtiles;
+  hgrp = rest % ng;
+  g = rest / ng;
+  mt = p.n_mtiles - 1 - mrev;
+  return true;
+}
+
+
+template <int D, bool CAUSAL, int OUT>
+__global__ void __launch_bounds__(256, 2)
+attn_bf16_pipe_kernel(AttnParams p) {
+  constexpr int BN = 64, NW = 4, NS = 2;    // keys per tile, waves, ring slots
+  constexpr int RB = D * 2;                 // bytes per key row
+  constexpr int NP = RB / 16;               // 16-byte pieces per row
+  constexpr int TB = BN * RB;               // bytes per tile
+  constexpr int LI = TB / 1024 / NW;        // direct-copy instructions per wave per tile (K or V)
+  constexpr int KS = D / 16, DB = D / 32;
+  constexpr int EPK = 32 / KS;              // exponentials per QK k-step
+  constexpr float TAU = 8.f;                // log2 bound on p under a lagging max
+  static_assert(LI >= 1 && TB % (1024 * NW) == 0, "tile must split into whole wave copies");
+  static_assert(LI <= 4, "the wait below counts at most 8 copies in flight");
+  // V swizzle: piece ^ 4*(row & 3) keeps the 4 rows x 4 pieces of a transposed
+  // read distinct (D = 64 has only 8 pieces per row: piece ^ 4*(row & 1)).
+  constexpr int VSW = NP >= 16 ? 3 : 1;
+  // One LDS object: K slots at s*TB, V slots at (NS+s)*TB. With a single
+  // object the compiler adds no wait of its own between a direct copy into one
+  // slot and reads of another.
+  __shared__ __attribute__((aligned(1024))) uint8_t kvl[2 * NS * TB];
+
+  int b, g, hgrp, mt;
+  if (!decode_work_hg(p, b, g, hgrp, mt)) return;
+  const int seq0 = p.cu[b];
+  const int len = p.cu[b + 1] - seq0;
+  const int bmw = 32 * p.P;                 // positions per workgroup
+  const int m0 = mt * bmw;
+  if (m0 >= len) return;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform: scalar branches
+  const int lq = lane & 31, hl = lane >> 5;
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const int h = g * p.G + hgrp * p.Hw + w % p.Hw;
+  const int wave_q0 = m0 + 32 * (w / p.Hw);
+  const int qi = wave_q0 + lq;
+  const uint32_t kvrow = (uint32_t)p.Hkv * RB;
+  const uint8_t* kbase = static_cast<const uint8_t*>(p.k) + ((size_t)seq0 * p.Hkv + g) * RB;
+  const uint8_t* vbase = static_cast<const uint8_t*>(p.v) + ((size_t)seq0 * p.Hkv + g) * RB;
+
+  // ---- per-lane constants
+  // Copy j of a wave moves 16-byte pieces of tile row ld_row[j]; its source
+  // is (tile base, wave-uniform) + ld_koff[j] / ld_voff[j] (per lane, fixed).
+  int ld_row[LI];
+  uint32_t ld_koff[LI], ld_voff[LI];
+#pragma unroll
+  for (int j = 0; j < LI; ++j) {
+    const int slot = (w + NW * j) * 64 + lane;
+    const int r = slot / NP, ph = slot % NP;
+    ld_row[j] = r;
+    ld_koff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ (r & (NP - 1))) * 16;
+    ld_voff[j] = (uint32_t)r * kvrow + (uint32_t)(ph ^ (4 * (r & VSW))) * 16;
+  }
+  const uint32_t lds_w = __builtin_amdgcn_readfirstlane((uint32_t)w * 1024u);  // this wave's copy slot
+  // K operand of S^T block nb: row 32*nb + swap23(lq), logical piece 2*ks + hl
+  // (block nb adds 32 rows; row & (NP-1) is unchanged for NP <= 32, so the
+  // swizzle of row 32*nb + rho equals that of rho)
+  const int rho = swap23(lq);
+  uint32_t koff[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) koff[ks] = rho * RB + (((2 * ks + hl) ^ (rho & (NP - 1))) * 16);
+  // V operand by transposed reads: lane reads row 16*kk + 8*(g16>>1) + 4*hf + (s16>>2),
+  // head-dim block c0 = 8*db + 4*(g16&1) + (s16&3) of 4 elements.
+  // (LDS byte addresses: the reads are inline assembly)
+  const int vrow0 = 8 * (g16 >> 1) + (s16 >> 2);
+  uint32_t voff[DB];
+  const uint32_t kvl_base =
+      (uint32_t)reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) uint8_t*)kvl);
+#pragma unroll
+  for (int db = 0; db < DB; ++db) {
+    const int c0 = 8 * db + 4 * (g16 & 1) + (s16 & 3);
+    voff[db] = kvl_base + vrow0 * RB + (((c0 >> 1) ^ (4 * (vrow0 & VSW))) * 16) + (c0 & 1) * 8;
+  }
+
+  const int kend = CAUSAL ? min(len, m0 + bmw) : len;
+  const int nt = (kend + BN - 1) / BN;
+
+  auto copy_rows = [&](const uint8_t* src, int tile, uint8_t* dst, const uint32_t* off) __attribute__((always_inline)) {
+    const int k0 = tile * BN;
+    const uint8_t* st = src + (size_t)k0 * kvrow;
+    // rows past the sequence end repeat its last key (no branch: the row
+    // shift is zero inside the sequence)
+    const int last = len - 1 - k0;
+#pragma unroll
+    for (int j = 0; j < LI; ++j) {
+      const uint32_t fix = (uint32_t)(min(ld_row[j], last) - ld_row[j]) * kvrow;
+      __builtin_amdgcn_global_load_lds((const void*)(st + (off[j] + fix)),
+                                       (__attribute__((address_space(3))) void*)(dst + lds_w + NW * j * 1024),
+                                       16, 0, 0);
+    }
+  };
+  auto copy_k = [&](int tile, auto slotc) __attribute__((always_inline)) {
+    copy_rows(kbase, tile, kvl + decltype(slotc)::value * TB, ld_koff);
+  };
+  auto copy_v = [&](int tile, auto slotc) __attribute__((always_inline)) {
+    copy_rows(vbase, tile, kvl + (NS + decltype(slotc)::value) * TB, ld_voff);
+  };
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+
+  bf16x8 qreg[KS];
+  {
+    const uint8_t* qr = static_cast<const uint8_t*>(p.q) + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * RB;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+      qreg[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qr + (ks * 16 + 8 * hl) * 2));
+  }
+  f32x16 o[DB];
+#pragma unroll
+  for (int db = 0; db < DB; ++db)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[db][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+  const float c = p.scale_log2;
+  const float tau_raw = TAU / c;  // TAU in raw logit units (c > 0)
+
+  // S^T blocks of a tile in a K slot: 2 x (32 keys x 32 queries),
+  // s[nb][r] = q(lane%32) . k(32*nb + swap23(acc_row32(r, hl))).
+  auto kread = [&](const uint8_t* kl, int ks, int nb) __attribute__((always_inline)) {
+    return __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(kl + nb * 32 * RB + koff[ks]));
+  };
+
+  // ---- prologue: Q, then K0, K1 and V0 landed
+  copy_k(0, S0{});
+  if (nt > 1) copy_k(1, S1{});
+  copy_v(0, S0{});
+  wait_vmcnt<0>();
+  lds_barrier();
+  f32x16 s[2];
+  {
+    const uint8_t* kl = kvl;
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[nb][r] = 0.f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        s[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kread(kl, ks, nb), qreg[ks], s[nb], 0, 0, 0);
+  }
+  lds_barrier();  // every wave has read K0: its slot may be refilled
+
+  // step t: S_t in s; K_{t+1} in K slot (U+1)%2, V_t in V slot U (U = t % 2);
+  // MORE: a tile t+1 exists (every step but the last)
+  auto step = [&](int t, auto uc, auto morec) __attribute__((always_inline)) {
+    constexpr int U = decltype(uc)::value;
+    constexpr bool MORE = decltype(morec)::value;
+    constexpr int UK1 = (U + 1) % NS;
+    const int k0 = t * BN;
+    // copies one step ahead of use: K_{t+2} into K_t's slot (read in step
+    // t-1), V_{t+1} into V_{t-1}'s slot
+    if (t + 2 < nt) copy_k(t + 2, std::integral_constant<int, U>{});
+    if (t + 1 < nt) copy_v(t + 1, std::integral_constant<int, UK1>{});
+    // ---- (a) mask (edge tiles only), row max, lazy rescale
+    const bool need_mask = (k0 + BN > len) || (CAUSAL && k0 + BN - 1 > wave_q0);
+    if (need_mask) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 32 * nb + swap23(acc_row32(r, hl));
+          if (key >= len || (CAUSAL && key > qi)) s[nb][r] = -INFINITY;
+        }
+    }
+    {
+      float mx = max32(s);
+      const float2 pr = pair_xor32(mx);
+      mx = __builtin_elementwise_maximum(pr.x, pr.y);
+      const bool grow = mx > m_run + tau_raw;
+      if (__any(grow)) {
+        const float m_new = grow ? mx : m_run;
+        const float alpha = (!grow) ? 1.f : (m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f((m_run - m_new) * c));
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) o[db][r] *= alpha;
+        m_run = m_new;
+      }
+    }
+    const float mc = m_run == -INFINITY ? 0.f : m_run * c;
+    // ---- (b) P_t = exp2(S_t*c - m*c), packed to bf16 as it is formed, with
+    // its row sum, under the MFMAs of S_{t+1}
+    uint32_t pk[16];  // bf16 pairs: pk[i] holds values 2i, 2i+1 of the lane's 32
+    float rsum[4] = {0.f, 0.f, 0.f, 0.f};
+    auto expo2 = [&](int i) __attribute__((always_inline)) {  // values 2i, 2i+1
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(s[(2 * i) >> 4][(2 * i) & 15], c, -mc));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(s[(2 * i + 1) >> 4][(2 * i + 1) & 15], c, -mc));
+      pk[i] = __builtin_bit_cast(uint32_t, bf16x2{(__bf16)e0, (__bf16)e1});
+      rsum[i & 3] += e0 + e1;
+    };
+    f32x16 sn[2];
+    if constexpr (MORE) {
+      const uint8_t* kl = kvl + UK1 * TB;
+      bf16x8 ka[2][2];
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) ka[0][nb] = kread(kl, 0, nb);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        if (ks + 1 < KS) {
+#pragma unroll
+          for (int nb = 0; nb < 2; ++nb) ka[(ks + 1) & 1][nb] = kread(kl, ks + 1, nb);
+        }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+          sn[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ka[ks & 1][nb], qreg[ks],
+                                                           ks == 0 ? f32x16{} : sn[nb], 0, 0, 0);
+#pragma unroll
+          for (int j = 0; j < EPK / 4; ++j) expo2((ks * EPK + nb * (EPK / 2)) / 2 + j);
+        }
+      }
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) expo2(i);
+    }
+    l_run += (rsum[0] + rsum[1]) + (rsum[2] + rsum[3]);
+    // ---- (c) O^T += V_t^T P_t^T. The transposed V reads of keys 0-31 are
+    // issued here, those of keys 32-63 once the first are in registers; each
+    // half is waited for before its MFMAs (the registers pass through the
+    // wait, so that no MFMA is placed before it).
+    uint32_t vaddr[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) vaddr[db] = voff[db] + (NS + U) * TB;
+    bf16x8 va0[DB], va1[DB];
+    auto pv = [&](int kk, bf16x8 (&va)[DB]) __attribute__((always_inline)) {
+      const bf16x8 pb = __builtin_bit_cast(bf16x8, u32x4{pk[4 * kk], pk[4 * kk + 1], pk[4 * kk + 2], pk[4 * kk + 3]});
+#pragma unroll
+      for (int db = 0; db < DB; ++db) o[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pb, o[db], 0, 0, 0);
+    };
+    vread_kk<RB, DB, 0>(va0, vaddr);
+    vread_kk<RB, DB, 1>(va1, vaddr);
+    lds_wait_n<2 * DB>(va0);
+    pv(0, va0);
+    vread_kk<RB, DB, 2>(va0, vaddr);
+    lds_wait_n<2 * DB>(va1);
+    pv(1, va1);
+    vread_kk<RB, DB, 3>(va1, vaddr);
+    lds_wait_n<2 * DB>(va0);
+    pv(2, va0);
+    lds_wait_n<0>(va1);
+    pv(3, va1);
+    // K_{t+2} and V_{t+1} have landed
+    wait_vmcnt<0>();
+    lds_barrier();
+    if constexpr (MORE) {
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb) s[nb] = sn[nb];
+    }
+  };
+  using Y = std::true_type;
+  // steps in pairs (ring slots 0, 1). The final step also forms the logits
+  // of a next tile from a stale slot; they are discarded.
+  for (int t = 0;; t += 2) {
+    step(t, S0{}, Y{});
+    if (t + 1 == nt) break;
+    step(t + 1, S1{}, Y{});
+    if (t + 2 == nt) break;
+  }
+
+  const float l = sum_xor32(l_run);
+  const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
+  if (qi < len) {
+    const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
+#pragma unroll
+    for (int db = 0; db < DB; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) store_out<OUT>(p.o, obase + db * 32 + acc_row32(r, hl), o[db][r] * inv);
+  }
+}
+
+
+// ---------------------------------------------------------------------------
 // E4M3 path: the bf16 kernel's structure on v_mfma_f32_32x32x64_f8f6f4. S^T
 // block nb holds keys 32*bit2(rho) + 16*nb + 4*(rho>>3) + (rho&3) in row rho, so
 // that a lane half's 32 accumulator values are keys 32*hl .. 32*hl+31, the B
@@ -663,6 +1023,19 @@ attn_fwd_f32_kernel(AttnParams p) {
 
 template <int D, bool CAUSAL, int OUT>
 static void launch_typed(const AttnArgs& a, AttnParams& p, hipStream_t stream) {
+  // bf16 grids of at most two 128-row workgroups per CU (256 CUs) take the
+  // pipelined loop: there the longest workgroup's chain of tiles sets the time
+  if (a.in_dtype == LITEVLM_BF16 &&
+      (long long)((a.max_seqlen + 127) / 128) * a.Hq * a.B <= 2LL * 256) {
+    p.Hw = p.G % 4 == 0 ? 4 : (p.G % 2 == 0 ? 2 : 1);
+    p.P = 4 / p.Hw;
+    const int bmp = 32 * p.P;
+    p.n_mtiles = (a.max_seqlen + bmp - 1) / bmp;
+    p.n_work = p.n_mtiles * (a.Hq / p.Hw) * a.B;
+    p.per_xcd = (p.n_work + 7) / 8;
+    hipLaunchKernelGGL((attn_bf16_pipe_kernel<D, CAUSAL, OUT>), dim3(8 * p.per_xcd), dim3(256), 0, stream, p);
+    return;
+  }
   const int bm = a.in_dtype == LITEVLM_F32 ? 64 : 128;
   p.n_mtiles = (a.max_seqlen + bm - 1) / bm;
   p.n_work = p.n_mtiles * a.Hq * a.B;
