@@ -1588,11 +1588,14 @@ void launch_gather(int B, int S, const int32_t* kept_index, const int32_t* cu_se
   };
   // 16-byte pieces per thread and row, (Q + K + V pieces) / 256: at most
   // (4096 + 2*4096) / 256 = 48 with Hq <= LITEVLM_MAX_HEADS (or a hidden-state
-  // row of up to 196 KB); about 24 loads in flight per thread
+  // row of up to 196 KB); about 12-24 loads in flight per thread. At 3 pieces
+  // (the 32/8-head, D = 128 bf16 rows) 4 rows per workgroup spread the rows
+  // over more workgroups than 8 did and measured faster (6 us at the batch-8
+  // workload, equal at batch 1).
   const int ppt = (qvec + 2 * kvvec + 255) / 256;
   if (ppt <= 1) launch(gather_rows_kernel<1, 8>, 8);
   else if (ppt <= 2) launch(gather_rows_kernel<2, 8>, 8);
-  else if (ppt <= 3) launch(gather_rows_kernel<3, 8>, 8);
+  else if (ppt <= 3) launch(gather_rows_kernel<3, 4>, 4);
   else if (ppt <= 4) launch(gather_rows_kernel<4, 6>, 6);
   else if (ppt <= 6) launch(gather_rows_kernel<6, 4>, 4);
   else if (ppt <= 12) launch(gather_rows_kernel<12, 2>, 2);
