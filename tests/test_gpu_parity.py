@@ -294,6 +294,24 @@ def test_fused_select_equals_two_calls(cfg, r):
         check_select(case, g, oracle.run_path(case, keep_ratio=r, attention=False), f"fused cfg{cfg}")
 
 
+@pytest.mark.parametrize("name,over", [
+    ("3 views of 43 (V_full = 129, not a multiple of 4), one masked, D=64",
+     dict(B=3, N=3, Tv=43, T=7, Hq=4, Hkv=2, D=64, n_masked=1, keep_ratio=0.4)),
+    ("one view", dict(B=2, N=1, Tv=100, T=9, Hq=8, Hkv=2, D=128, n_masked=0, keep_ratio=0.5)),
+    ("8 views of 24, up to 4 masked", dict(B=4, N=8, Tv=24, T=5, Hq=8, Hkv=8, D=128, n_masked=4, keep_ratio=0.7)),
+])
+def test_fused_select_view_layouts(name, over):
+    """View boundaries off the 4-key vectors and the 64-key tiles, a single
+    view, the most views the in-call selection takes: bit for bit the two-call
+    path, and the oracle's selection."""
+    case = synth.config_case(2, **over)
+    log(f"fused select {name}: B={case.B} N={case.N} V_full={case.V_full} S={case.S}")
+    g = run_fused(case)
+    two = run_two_calls(case, case.keep_ratio, case.view_logit, None, case.w_lexical, case.threshold)
+    assert_same_select(g, two, name)
+    check_select(case, g, oracle.run_path(case, attention=False), name)
+
+
 def test_fused_select_random_logits_lexical_fallback():
     """Logits near the threshold, lexical scores, and samples where no view
     passes (the best-view fallback): the in-call decision is the patch-select
