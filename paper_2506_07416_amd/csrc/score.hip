@@ -34,6 +34,8 @@ constexpr int kSweepWaves = 16;             // waves per sweep-1 workgroup, 32 q
 constexpr int kSweepThreads = 64 * kSweepWaves;
 constexpr int RBLK = 32 * kSweepWaves;      // query rows per sweep-1 workgroup
 constexpr int kMaxSplitTiles = 64;          // key tiles per split (one 64-bit live mask)
+constexpr int kBalMaxBatch = kSweepWaves;   // balanced sweep-1 split: one wave per sample
+constexpr int kBalWords = 4;                // ... and at most 256 key tiles per sample
 constexpr int kLdsBytes = 160 * 1024;       // LDS of a workgroup (gfx950)
 // sweep 2
 constexpr int KW = 64;                      // keys per wave: 2 blocks of 32
@@ -53,12 +55,18 @@ constexpr unsigned long long kDroppedCol = ~0ull;
 struct ScoreSplit {
   int n_rb, n_kt, ns1;      // sweep 1: row blocks of RBLK rows, key tiles of KB keys, key splits
   int n_vt, nchunks, rs2;   // sweep 2: visual key tiles of KT keys, row chunks of CH rows, row splits
+  int ns1_slots;            // sweep-1 partials per (sample, KV group, row): ns1, or 2*ns1 where a
+                            // balanced split may give a sample more splits than ns1
 };
 
 struct ScoreDims {
   int B, S, V_full, T, Hq, Hkv, G, R;
   int tq0;  // the query rows are text tokens tq0 .. tq0 + T - 1 (the last T of them)
+  // ns1: partials per (sample, KV group, row), the split count unless bal.
+  // bal: sweep 1 splits each sample's live key tiles, ns1u splits per column
+  // on average (the grid), at most ns1 for one sample.
   int n_rb, n_kt, ns1, n_vt, nchunks, rs2;
+  int bal, ns1u;
   float scale_log2;
   float fx;  // fixed-point scale of the column sums (a power of two)
   // in-call patch selection (the kernels' VSEL instances): keep flags from the
@@ -109,12 +117,165 @@ __device__ __forceinline__ bool decode_column(int ncol, int nsplit, int& col, in
   return true;
 }
 
+// (sample, KV group) pair at position i of an order that deals the pairs to
+// the 8 XCDs round-robin: the XCD-contiguous column ranges then hold pairs x,
+// x+8, x+16, ..., so every XCD gets a share of every sample.
+__device__ __forceinline__ int pair_at(int i, int npair) {
+  const int q = npair >> 3, m = npair & 7;
+  if (i < m * (q + 1)) {
+    const int r = i / (q + 1);
+    return r + 8 * (i - r * (q + 1));
+  }
+  const int i2 = i - m * (q + 1), r = m + i2 / q;
+  return r + 8 * (i2 - (r - m) * q);
+}
+
 // First key tile of split `split` of n tiles in ns splits: the first n % ns
 // splits take one tile more, so the last split (text keys, masked) is never
 // the long one.
 __device__ __forceinline__ int split_begin(int split, int n, int ns) {
   const int base = n / ns, rem = n - base * ns;
   return split * base + min(split, rem);
+}
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i(int x) {
+  return __builtin_amdgcn_update_dpp(0, x, CTRL, 0xF, 0xF, false);
+}
+
+// Balanced sweep-1 split over samples with unequal numbers of live key tiles
+// (tiles holding a key that some row sees: a key of a kept view, or a text
+// key), with the view selection inside the call.
+//  1. Wave b evaluates sample b's view mask and marks its live tiles.
+//  2. Wave 0 gives sample b ns_b = max(1, ceil(nl_b / tau)) splits per column
+//     (nl_b live tiles), for the smallest tau in [1, 64] whose splits fit the
+//     grid's B*ns1u per column, with at most ns1 for one sample, and takes the
+//     workgroup's unit from the order (sample, KV group, row block, split),
+//     each XCD a contiguous range of it.
+//  3. Split s of a column takes the live tiles of ranks [a, a + ntl) (the
+//     first nl_b % ns_b splits one more), and lane j of `list` returns the
+//     j-th of them.
+// LDS `tmp` (1 KB) is free for the workgroup on entry and again on return.
+// Returns false for a workgroup without a unit; every thread returns the same.
+struct BalUnit {
+  int b, g, rb, split, ntl, ns;
+  int list;
+};
+
+__device__ bool bal_unit(const ScoreDims& d, uint8_t* tmp, int w, int lane, BalUnit& u) {
+  uint64_t* lm = reinterpret_cast<uint64_t*>(tmp);                      // [kBalMaxBatch][kBalWords]
+  int* nl = reinterpret_cast<int*>(tmp + 8 * kBalMaxBatch * kBalWords);  // [kBalMaxBatch]
+  int* res = nl + kBalMaxBatch;                                          // b, g, rb, split, ntl, ns, a, valid
+  int* lst = res + 8;                                                    // [64]
+  if (w < d.B) {
+    const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(view_load(d.vs.logit, d.vs.lexical, d.vs.N, w, lane),
+                                                               d.vs.lexical != nullptr, d.vs.w, d.vs.tau, d.vs.N,
+                                                               lane);
+    int cnt = 0;
+#pragma unroll
+    for (int wd = 0; wd < kBalWords; ++wd) {
+      const int t = 64 * wd + lane, k0 = KB * t, k1 = k0 + KB;
+      uint32_t live = k1 > d.V_full ? 1u : 0u;  // holds a text key
+#pragma unroll
+      for (int v = 0; v < kFusedViews; ++v)  // bitwise, no branches: a kept view overlaps the tile
+        live |= (v < d.vs.N ? 1u : 0u) & (vm >> v) & (d.vs.off[v] < k1 ? 1u : 0u) & (d.vs.off[v + 1] > k0 ? 1u : 0u);
+      const uint64_t bits = __ballot((live & (t < d.n_kt ? 1u : 0u)) != 0u);
+      cnt += __popcll(bits);
+      if (lane == 0) lm[w * kBalWords + wd] = bits;
+    }
+    if (lane == 0) nl[w] = cnt;
+  }
+  __syncthreads();
+  if (w == 0) {
+    // lane b < B (all in the wave's first row of 16 lanes): sample b's live
+    // tiles and splits per column; sums, maxima and prefixes over the samples
+    // by row-of-16 DPP, read back with readlane (no LDS round trips)
+    const int nlb = lane < d.B ? nl[lane] : 0;
+    const int budget = d.B * d.ns1u;
+    // ceil(n / t) for 0 <= n <= 256, 1 <= t <= 256: the float quotient is within
+    // an ulp of the exact one, so its ceiling is off by at most one, corrected
+    auto ceil_div = [](int n, int t) {
+      int q = (int)ceilf(__fdividef((float)n, (float)t));
+      q -= (q - 1) * t >= n ? 1 : 0;
+      q += q * t < n ? 1 : 0;
+      return q;
+    };
+    auto splits = [&](int tau) { return lane < d.B ? max(1, ceil_div(nlb, tau)) : 0; };
+    auto samples_sum = [](int x) {
+      x += dpp_i<0xB1>(x);   // quad_perm [1,0,3,2]
+      x += dpp_i<0x4E>(x);   // quad_perm [2,3,0,1]
+      x += dpp_i<0x141>(x);  // row_half_mirror
+      x += dpp_i<0x140>(x);  // row_mirror
+      return __builtin_amdgcn_readfirstlane(x);
+    };
+    auto samples_max = [](int x) {
+      x = max(x, dpp_i<0xB1>(x));
+      x = max(x, dpp_i<0x4E>(x));
+      x = max(x, dpp_i<0x141>(x));
+      x = max(x, dpp_i<0x140>(x));
+      return __builtin_amdgcn_readfirstlane(x);
+    };
+    // tau >= ceil(nl_b / ns1) keeps every sample within ns1 splits; tau = 64
+    // fits the budget, since ns1u >= ceil(n_kt / 64) >= ceil(nl_b / 64)
+    int lo = samples_max(lane < d.B ? ceil_div(nlb, d.ns1) : 1);
+    int hi = 64;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (samples_sum(splits(mid)) <= budget) hi = mid;
+      else lo = mid + 1;
+    }
+    const int nsb = splits(lo);
+    const int C = d.Hkv * d.n_rb;  // columns per sample
+    // inclusive prefix of the units C*ns_b over the samples (row_shr 1, 2, 4, 8)
+    int incl = C * nsb;
+    incl += dpp_i<0x111>(incl);
+    incl += dpp_i<0x112>(incl);
+    incl += dpp_i<0x114>(incl);
+    incl += dpp_i<0x118>(incl);
+    const int total = __builtin_amdgcn_readlane(incl, 15);
+    const int L = blockIdx.x, x = L & 7, j = L >> 3;
+    const int u0 = (int)(((long long)x * total) >> 3), u1 = (int)(((long long)(x + 1) * total) >> 3);
+    const bool valid = j < u1 - u0;
+    const int unit = u0 + j;
+    // sample b: the lane whose prefix range holds the unit
+    const uint64_t hit = __ballot(valid && lane < d.B && unit < incl && unit >= incl - C * nsb);
+    const int b = hit ? (int)__builtin_ctzll(hit) : 0;
+    const int ns = __builtin_amdgcn_readlane(nsb, b), base = __builtin_amdgcn_readlane(incl, b) - C * ns;
+    const int nlv = __builtin_amdgcn_readlane(nlb, b);
+    const int r = unit - base, col = r / max(ns, 1), split = r - col * ns;
+    const int a = split_begin(split, nlv, ns), ntl = split_begin(split + 1, nlv, ns) - a;
+    if (lane == 0) {
+      res[0] = b;
+      res[1] = col / d.n_rb;
+      res[2] = col - (col / d.n_rb) * d.n_rb;
+      res[3] = split;
+      res[4] = ntl;
+      res[5] = ns;
+      res[7] = valid && hit ? 1 : 0;
+    }
+    // the split's tiles: the live tile of rank a + i goes to entry i (ranks
+    // from the lanes below in the same word plus the words before)
+    lst[lane] = 0;
+    int rank0 = 0;
+#pragma unroll
+    for (int wd = 0; wd < kBalWords; ++wd) {
+      const uint64_t m = lm[b * kBalWords + wd];
+      const int rank = rank0 + (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+      if (((m >> lane) & 1ull) && rank >= a && rank < a + ntl) lst[rank - a] = 64 * wd + lane;
+      rank0 += __popcll(m);
+    }
+  }
+  __syncthreads();
+  u.b = res[0];
+  u.g = res[1];
+  u.rb = res[2];
+  u.split = res[3];
+  u.ntl = res[4];
+  u.ns = res[5];
+  const bool valid = res[7] != 0;
+  u.list = lst[lane];
+  __syncthreads();  // tmp is read by every wave before the caller reuses it
+  return valid;
 }
 
 // ---------------------------------------------------------------- sweep-1 logit tiles
@@ -293,16 +454,21 @@ struct KeyPipe {
   const uint8_t* kg;  // key 0 of this sample and KV head
   size_t kvrow;
   int tile0, ntl, klim, w, lane, cpw;
+  int list;  // with a balanced split: lane j holds the split's j-th key tile
+  bool bal;
 
-  __device__ __forceinline__ KeyPipe(uint8_t* r, const uint8_t* k, size_t kv, int t0, int n, int lim, int w_, int l)
-      : ring(r), kg(k), kvrow(kv), tile0(t0), ntl(n), klim(lim), w(w_), lane(l) {
+  __device__ __forceinline__ KeyPipe(uint8_t* r, const uint8_t* k, size_t kv, int t0, int n, int lim, int w_, int l,
+                                     int list_, bool bal_)
+      : ring(r), kg(k), kvrow(kv), tile0(t0), ntl(n), klim(lim), w(w_), lane(l), list(list_), bal(bal_) {
     cpw = w < IPC ? (IPC - 1 - w) / kSweepWaves + 1 : 0;  // this wave's copies per tile
   }
+  // key tile of step t (0 <= t < ntl <= 64)
+  __device__ __forceinline__ int tile(int t) const { return bal ? __builtin_amdgcn_readlane(list, t) : tile0 + t; }
   __device__ __forceinline__ const uint8_t* buf(int t) const { return ring + (t % NB) * Tile::TILE; }
   __device__ __forceinline__ void issue(int t) {
     if (t >= ntl) return;
     uint8_t* dst = ring + (t % NB) * Tile::TILE;
-    const int key0 = (tile0 + t) * KB;
+    const int key0 = tile(t) * KB;
     for (int sub = w; sub < IPC; sub += kSweepWaves) {
       const int slot = sub * 64 + lane;
       const int row = slot / Tile::NP, ph = slot - row * Tile::NP;
@@ -346,7 +512,8 @@ __device__ __forceinline__ void load_keep_bytes(const uint8_t* keep_row, int til
   }
 }
 
-__device__ __forceinline__ void tile_flags(uint64_t* mw, uint8_t* keepl, const uint8_t f[kFlagsPer], int tile0,
+template <class Pipe>
+__device__ __forceinline__ void tile_flags(uint64_t* mw, uint8_t* keepl, const uint8_t f[kFlagsPer], const Pipe& pipe,
                                            int ntl, int V_full, int limit, int w, int lane, uint64_t& live,
                                            uint64_t& plain) {
   // each wave writes the bits of its own tiles into its own words; no atomics
@@ -354,7 +521,7 @@ __device__ __forceinline__ void tile_flags(uint64_t* mw, uint8_t* keepl, const u
 #pragma unroll
   for (int i = 0; i < kFlagsPer; ++i) {
     const int j = w + kSweepWaves * i;
-    const int key = (tile0 + j) * KB + lane;
+    const int key = pipe.tile(j) * KB + lane;
     const bool vis = key < V_full && f[i] != 0;
     const bool txt = key >= V_full && key < limit;
     const uint64_t lv = __ballot(vis || txt), pl = __ballot(vis);
@@ -443,17 +610,44 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   uint8_t* keepl = lds + FOFF;
   uint64_t* mw = reinterpret_cast<uint64_t*>(keepl + kMaxSplitTiles * KB);
 
-  // the column sums of sweep 2 start from zero (this grid runs before it)
-  for (int i = blockIdx.x * kSweepThreads + threadIdx.x; i < d.B * d.V_full; i += gridDim.x * kSweepThreads)
-    acc[i] = 0ull;
+  // the column sums of sweep 2 start from zero (this grid runs before it);
+  // after the work decode: loads wait for the stores issued before them
+  auto zero_acc = [&]() {
+    for (int i = blockIdx.x * kSweepThreads + threadIdx.x; i < d.B * d.V_full; i += gridDim.x * kSweepThreads)
+      acc[i] = 0ull;
+  };
 
-  int col, split;
-  if (!decode_column(d.B * d.Hkv * d.n_rb, d.ns1, col, split)) return;
-  const int bg = col / d.n_rb, rb = col - bg * d.n_rb;
-  const int b = bg / d.Hkv, g = bg - b * d.Hkv;
-  const int tile0 = split_begin(split, d.n_kt, d.ns1);
-  const int ntl = split_begin(split + 1, d.n_kt, d.ns1) - tile0;
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  int b, g, rb, split, tile0 = 0, ntl, list = 0, nsb = 0;
+  bool bal = false;
+  if constexpr (VSEL) bal = d.bal != 0;
+  if (bal) {
+    BalUnit u;
+    if (!bal_unit(d, lds, w, lane, u)) {
+      zero_acc();
+      return;
+    }
+    b = u.b;
+    g = u.g;
+    rb = u.rb;
+    split = u.split;
+    ntl = u.ntl;
+    nsb = u.ns;
+    list = u.list;
+  } else {
+    int col;
+    if (!decode_column(d.B * d.Hkv * d.n_rb, d.ns1, col, split)) {
+      zero_acc();
+      return;
+    }
+    const int bg = col / d.n_rb;
+    rb = col - bg * d.n_rb;
+    b = bg / d.Hkv;
+    g = bg - b * d.Hkv;
+    tile0 = split_begin(split, d.n_kt, d.ns1);
+    ntl = split_begin(split + 1, d.n_kt, d.ns1) - tile0;
+  }
+  zero_acc();
   const int lq = lane & 31, hl = lane >> 5;
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * d.S : nullptr;
   const uint8_t* q = static_cast<const uint8_t*>(qv);
@@ -484,7 +678,7 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   // completing in order, for everything before them).
   Tile tile;
   KeyPipe<Tile> pipe(lds, k + ((size_t)b * d.S * d.Hkv + g) * Tile::RB, (size_t)d.Hkv * Tile::RB, tile0, ntl,
-                     d.S, w, lane);
+                     d.S, w, lane, list, bal);
 #pragma unroll
   for (int t = 0; t < (Tile::QSTAGE ? NPRE : Tile::NBUF - 1); ++t) pipe.issue(t);
   if (Tile::QSTAGE) q_round(0);
@@ -515,12 +709,12 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
     const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(vin, d.vs.lexical != nullptr, d.vs.w, d.vs.tau, d.vs.N, lane);
 #pragma unroll
     for (int i = 0; i < kFlagsPer; ++i) {
-      const int key = (tile0 + w + kSweepWaves * i) * KB + lane;
+      const int key = pipe.tile(w + kSweepWaves * i) * KB + lane;
       kf[i] = d.V_full > 0 ? (uint8_t)view_token_flag(d.vs, vm, min(key, d.V_full - 1)) : 1;
     }
   }
   uint64_t live, plain;
-  tile_flags(mw, keepl, kf, tile0, ntl, d.V_full, d.S, w, lane, live, plain);
+  tile_flags(mw, keepl, kf, pipe, ntl, d.V_full, d.S, w, lane, live, plain);
 
   // token of the lane's row for the causal text mask (-1: a row past R sees no text)
   const int t_row = row < d.R ? d.tq0 + row / d.G : -1;
@@ -531,7 +725,7 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   auto stats = [&](int t, f32x16* s) __attribute__((always_inline)) {
     if (!((plain >> t) & 1ull)) {
       // visible: kept visual keys, and text keys V_full + t' with t' <= the row's token
-      const int key0 = (tile0 + t) * KB;
+      const int key0 = pipe.tile(t) * KB;
       const int ns = keys_upto(d.S - 1 - key0 - 4 * hl);        // keys < S
       const int n1 = min(keys_upto(d.V_full + t_row - key0 - 4 * hl), ns);
       const uint32_t below_n1 = n1 >= 32 ? 0xFFFFFFFFu : ((1u << n1) - 1u);
@@ -590,9 +784,13 @@ score_rowstats_kernel(ScoreDims d, const void* __restrict__ qv, const void* __re
   if (wave_active && lag && ((live >> (ntl - 1)) & 1ull)) stats(ntl - 1, s);
   // both lane halves share the running max; their sums cover different keys
   const float z = sum_xor32(z_run);
-  if (hl == 0 && row < d.R)
-    rowpart[(((size_t)b * d.Hkv + g) * d.ns1 + split) * d.R + row] =
-        make_float2(m_run == -INFINITY ? -INFINITY : m_run * c, z);
+  if (hl == 0 && row < d.R) {
+    float2* rp = rowpart + ((size_t)b * d.Hkv + g) * d.ns1 * d.R + row;
+    rp[(size_t)split * d.R] = make_float2(m_run == -INFINITY ? -INFINITY : m_run * c, z);
+    // a balanced split fills the partials of the splits its sample does not use
+    if (bal && split == 0)
+      for (int sl = nsb; sl < d.ns1; ++sl) rp[(size_t)sl * d.R] = make_float2(-INFINITY, 0.f);
+  }
 }
 
 // ---------------------------------------------------------------- sweep-2 logit tiles
@@ -867,7 +1065,8 @@ score_colmass_kernel(ScoreDims d, const void* __restrict__ qv, const void* __res
 
   int col, rs;
   if (!decode_column(d.B * d.Hkv * d.n_vt, d.rs2, col, rs)) return;
-  const int bg = col / d.n_vt, vt = col - bg * d.n_vt;
+  const int bgi = col / d.n_vt, vt = col - bgi * d.n_vt;
+  const int bg = pair_at(bgi, d.B * d.Hkv);
   const int b = bg / d.Hkv, g = bg - b * d.Hkv;
   const uint8_t* q = static_cast<const uint8_t*>(qv);
   const uint8_t* k = static_cast<const uint8_t*>(kv);
@@ -1464,6 +1663,14 @@ gather_rows_kernel(int B, int S, const int32_t* __restrict__ kept_index,
 
 static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Shapes where sweep 1 may split unevenly over the samples (with the view
+// selection inside the call): more than one sample, at most one per wave of
+// the workgroup, at least two splits per column to move, and every sample's
+// live tiles in kBalWords words.
+static bool bal_shape(int B, int ns1, int n_kt) {
+  return B > 1 && B <= kBalMaxBatch && ns1 >= 2 && n_kt <= 64 * kBalWords;
+}
+
 static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv, int n_query) {
   // Sweep 1: one 16-wave workgroup per CU (256 CUs); the key tiles of each
   // (sample, KV group, row block) are split until the grid has ~256
@@ -1479,11 +1686,13 @@ static ScoreSplit score_split(int B, int S, int V_full, int Hq, int Hkv, int n_q
   const long long cols = std::max<long long>(1, (long long)B * Hkv * p.n_rb);
   const int want = (int)std::max<long long>(1, 256 / cols);
   p.ns1 = std::max((p.n_kt + kMaxSplitTiles - 1) / kMaxSplitTiles, std::min(p.n_kt, want));
+  p.ns1_slots = bal_shape(B, p.ns1, p.n_kt) ? 2 * p.ns1 : p.ns1;
   p.n_vt = (V_full + KT - 1) / KT;
   p.nchunks = (R + CH - 1) / CH;
   const long long c2 = (long long)p.n_vt * Hkv * B;
   const int fit = c2 == 0 ? 1 : (int)std::min<long long>(std::min(p.nchunks, 4), std::max<long long>(1, 768 / c2));
   p.rs2 = std::max(fit, (p.nchunks + kMaxChunksPerSplit - 1) / kMaxChunksPerSplit);
+  if (c2 > 768) p.rs2 = std::max(p.rs2, std::min(p.nchunks, 2));
   return p;
 }
 
@@ -1492,7 +1701,7 @@ ScoreWorkspace score_workspace_layout(int B, int S, int V_full, int Hq, int Hkv,
   const size_t R = (size_t)(Hq / Hkv) * n_query;
   ScoreWorkspace w;
   w.rowpart_off = 0;
-  w.acc_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1 * R);
+  w.acc_off = align256(w.rowpart_off + sizeof(float2) * B * Hkv * (size_t)sp.ns1_slots * R);
   w.total = align256(w.acc_off + sizeof(unsigned long long) * B * (size_t)V_full);
   return w;
 }
@@ -1537,7 +1746,11 @@ hipError_t launch_token_score_topk(const ScoreArgs& a, hipStream_t stream) {
   d.R = d.G * d.T;
   d.n_rb = sp.n_rb;
   d.n_kt = sp.n_kt;
-  d.ns1 = sp.ns1;
+  // with the view selection inside the call, every workgroup can find the
+  // live tiles of every sample, and sweep 1 splits them evenly
+  d.bal = a.vs.N > 0 && bal_shape(a.B, sp.ns1, sp.n_kt) ? 1 : 0;
+  d.ns1u = sp.ns1;
+  d.ns1 = d.bal ? sp.ns1_slots : sp.ns1;
   d.n_vt = sp.n_vt;
   d.nchunks = sp.nchunks;
   d.rs2 = sp.rs2;

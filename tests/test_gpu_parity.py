@@ -264,15 +264,50 @@ def run_two_calls(case, keep_ratio, logit, lexical, w, tau):
                 kept_index=out["kept_index"][:cu[-1]].cpu().numpy(), dev=out)
 
 
-def assert_same_select(a, b, label):
-    """Every output of two selection runs bit for bit (the packed rows up to cu[B])."""
-    for key in ("view_keep", "token_keep", "n_vis", "cu", "kept_index"):
+def balanced_split(case):
+    """True where the in-call selection splits sweep 1's key tiles unevenly
+    over the samples (their live tiles follow the view masks), so that its
+    row partials, and the scores' last bits, differ from the two-call path's:
+    more than one sample, at most 16, at least two key splits per (sample, KV
+    group, row block), at most 256 key tiles of 64."""
+    R = (case.Hq // case.Hkv) * (case.S - case.V_full)
+    n_rb = -(-R // 512)
+    n_kt = -(-case.S // 64)
+    ns1 = max(-(-n_kt // 64), min(n_kt, max(1, 256 // (case.B * case.Hkv * n_rb))))
+    return 1 < case.B <= 16 and ns1 >= 2 and n_kt <= 256
+
+
+def assert_same_select(a, b, label, case, exact=True):
+    """Two selection runs (a: the in-call selection, b: the two calls) agree.
+    exact: every output bit for bit (the packed rows up to cu[B]). Otherwise
+    the view decision, the lengths and the text tails bit for bit, the scores
+    within SCORE_RTOL of each other, a's kept set by the band rule around b's
+    scores, and a's packed rows exact copies of the inputs at a's indices."""
+    for key in ("view_keep", "token_keep", "n_vis", "cu"):
         assert np.array_equal(a[key], b[key]), f"{label}: {key}"
-    assert np.array_equal(a["scores"].astype(np.float32).view(np.uint32),
-                          b["scores"].astype(np.float32).view(np.uint32)), f"{label}: scores"
-    rows = int(a["cu"][-1])
-    for name in ("qc", "kc", "vc"):
-        assert torch.equal(bits_of_t(a["dev"][name][:rows]), bits_of_t(b["dev"][name][:rows])), f"{label}: {name}"
+    if exact:
+        assert np.array_equal(a["kept_index"], b["kept_index"]), f"{label}: kept_index"
+        assert np.array_equal(a["scores"].astype(np.float32).view(np.uint32),
+                              b["scores"].astype(np.float32).view(np.uint32)), f"{label}: scores"
+        rows = int(a["cu"][-1])
+        for name in ("qc", "kc", "vc"):
+            assert torch.equal(bits_of_t(a["dev"][name][:rows]), bits_of_t(b["dev"][name][:rows])), f"{label}: {name}"
+        return
+    err = score_rel_err(b["scores"], a["scores"])
+    assert err <= SCORE_RTOL, f"{label}: in-call vs two-call score rel err {err:.3g}"
+    same = 0
+    for bb in range(case.B):
+        seg = a["kept_index"][a["cu"][bb]:a["cu"][bb + 1]]
+        k_b = seg.shape[0] - (case.S - case.V_full)
+        assert np.array_equal(seg[k_b:], np.arange(case.V_full, case.S)), f"{label}: text tail"
+        ok, _ = check_selection(b["scores"][bb], b["token_keep"][bb], case.V_full, k_b, seg[:k_b])
+        same += int(ok)
+    for name, src in (("qc", case.q), ("kc", case.k), ("vc", case.v)):
+        got = bits_of(a["dev"][name][:a["cu"][-1]])
+        want = np.concatenate([src[bb, a["kept_index"][a["cu"][bb]:a["cu"][bb + 1]]] for bb in range(case.B)])
+        assert np.array_equal(got.reshape(want.shape).view(want.dtype), want), f"{label}: {name} bits"
+    log(f"{label}: balanced split, scores within {err:.2e} of the two calls, "
+        f"{same} of {case.B} kept sets identical")
 
 
 def bits_of_t(t):
@@ -289,8 +324,9 @@ def test_fused_select_equals_two_calls(cfg, r):
     log(f"fused select cfg{cfg}: B={case.B} S={case.S} N={case.N} {case.dtype} r={r}")
     g = run_fused(case, keep_ratio=r)
     two = run_two_calls(case, r, case.view_logit, None, case.w_lexical, case.threshold)
-    assert_same_select(g, two, f"cfg{cfg}")
-    if cfg in (1, 2):
+    exact = not balanced_split(case)
+    assert_same_select(g, two, f"cfg{cfg}", case, exact)
+    if cfg in (1, 2) or not exact:
         check_select(case, g, oracle.run_path(case, keep_ratio=r, attention=False), f"fused cfg{cfg}")
 
 
@@ -308,7 +344,7 @@ def test_fused_select_view_layouts(name, over):
     log(f"fused select {name}: B={case.B} N={case.N} V_full={case.V_full} S={case.S}")
     g = run_fused(case)
     two = run_two_calls(case, case.keep_ratio, case.view_logit, None, case.w_lexical, case.threshold)
-    assert_same_select(g, two, name)
+    assert_same_select(g, two, name, case, not balanced_split(case))
     check_select(case, g, oracle.run_path(case, attention=False), name)
 
 
@@ -327,7 +363,7 @@ def test_fused_select_random_logits_lexical_fallback():
     for w, tau, lx in ((0.0, tau0, None), (0.3, 0.55, lex), (1.0, 0.7, lex), (0.0, 0.999, None)):
         g = run_fused(case, logit=logit, lexical=lx, w=w, tau=tau)
         two = run_two_calls(case, case.keep_ratio, logit, lx, w, tau)
-        assert_same_select(g, two, f"w={w} tau={tau}")
+        assert_same_select(g, two, f"w={w} tau={tau}", case, not balanced_split(case))
         n_band = check_view_keep(oracle.view_scores(logit, lx, w), tau, g["view_keep"])
         log(f"fused w={w} tau={tau}: views kept {int(g['view_keep'].sum())} of {case.B * case.N}, "
             f"{n_band} in the threshold band")
