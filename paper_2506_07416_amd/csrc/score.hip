@@ -1299,12 +1299,16 @@ __device__ __forceinline__ int wave_count_flags(const uint8_t* row, int n, int l
 // barrier. Returns the exclusive prefix; *total gets the block total.
 __device__ __forceinline__ int block_scan_excl(int v, int* wsum, int* total) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // inclusive wave scan on DPP: within rows of 16 (row_shr 1, 2, 4, 8), then
+  // row 0's last lane into row 1 and row 2's into row 3 (row_bcast:15), then
+  // lane 31 into rows 2 and 3 (row_bcast:31)
   int x = v;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const int y = __shfl_up(x, off, kWave);
-    if (lane >= off) x += y;
-  }
+  x += dpp_i<0x111>(x);
+  x += dpp_i<0x112>(x);
+  x += dpp_i<0x114>(x);
+  x += dpp_i<0x118>(x);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x142, 0xA, 0xF, false);
+  x += __builtin_amdgcn_update_dpp(0, x, 0x143, 0xC, 0xF, false);
   if (lane == 63) wsum[wave] = x;
   __syncthreads();
   int before = 0, tot = 0;
@@ -1350,8 +1354,13 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   // kept-visual counts below.
   const uint8_t* keep_row = token_keep ? token_keep + (size_t)b * S : nullptr;
   // the sample's view selection, requested first (its mask gives every keep flag)
-  ViewIn vin;
-  if constexpr (VSEL) vin = view_load(vs.logit, vs.lexical, vs.N, b, lane);
+  // and the view scores of sample `wave` (<= b), whose kept-visual count
+  // enters this sample's offset
+  ViewIn vin, vinw;
+  if constexpr (VSEL) {
+    vin = view_load(vs.logit, vs.lexical, vs.N, b, lane);
+    vinw = view_load(vs.logit, vs.lexical, vs.N, min(wave, b), lane);
+  }
   const unsigned long long* ac = acc + (size_t)b * V_full;
   float* sc = scores + (size_t)b * V_full;
   auto score_of = [&](unsigned long long v, bool kept) { return kept ? (float)((double)v * inv) : -INFINITY; };
@@ -1384,6 +1393,7 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
     const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(vin, vs.lexical != nullptr, vs.w, vs.tau, vs.N, lane);
     if (view_keep_out && tid < vs.N) view_keep_out[(size_t)b * vs.N + tid] = (uint8_t)((vm >> tid) & 1u);
     uint8_t* row = token_keep_out ? token_keep_out + (size_t)b * S : nullptr;
+    const bool row4 = (reinterpret_cast<uintptr_t>(row) & 3) == 0;  // 4 flags per store
     if (vec) {
 #pragma unroll
       for (int i = 0; i < R4; ++i) {
@@ -1394,8 +1404,12 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
         f4[i] = f;
         const int j4 = 4 * (tid + i * kTopkThreads);
         if (row && j4 < V_full) {
+          if (row4) {
+            *reinterpret_cast<uint32_t*>(row + j4) = f;
+          } else {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) row[j4 + u] = (uint8_t)((f >> (8 * u)) & 1u);
+            for (int u = 0; u < 4; ++u) row[j4 + u] = (uint8_t)((f >> (8 * u)) & 1u);
+          }
         }
       }
     } else if (row) {
@@ -1409,8 +1423,8 @@ topk_compact_kernel(int S, int V_full, double keep_ratio, const uint8_t* __restr
   for (int bb = wave; bb <= b; bb += kTopkWaves) {
     int c;
     if constexpr (VSEL) {
-      const uint32_t m = (uint32_t)view_keep_mask<kFusedViews>(view_load(vs.logit, vs.lexical, vs.N, bb, lane),
-                                                  vs.lexical != nullptr, vs.w, vs.tau, vs.N, lane);
+      const ViewIn vi = bb == wave ? vinw : view_load(vs.logit, vs.lexical, vs.N, bb, lane);
+      const uint32_t m = (uint32_t)view_keep_mask<kFusedViews>(vi, vs.lexical != nullptr, vs.w, vs.tau, vs.N, lane);
       c = 0;
       for (int v = 0; v < vs.N; ++v) c += ((m >> v) & 1u) ? vs.off[v + 1] - vs.off[v] : 0;
     } else {
