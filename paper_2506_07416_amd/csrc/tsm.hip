@@ -22,9 +22,13 @@
 // (66 KB, two workgroups per CU) into 128-byte rows whose 16-byte pieces are
 // XOR-swizzled so that operand reads are free of bank conflicts. Measured
 // alternatives (256-row or 256-feature tiles, 3- to 6-stage rings, 32-column
-// stages) were slower on both the batch-1 and the batch-8 shapes: the workgroups
-// wait on the copies, and what helps is more workgroups per CU, not deeper
-// rings.
+// stages, four workgroups per CU with 32-column stages) were slower or equal on
+// both the batch-1 and the batch-8 shapes.
+//
+// Epilogue: the rotation angle is reduced to [-1/2, 1/2] turns in double and
+// taken by the hardware sine and cosine (which work in turns), and the rotated
+// tile is staged through the free ring as bf16 rows so that it leaves in
+// 16-byte stores of whole rows; the accumulators hold one feature per lane.
 #include <type_traits>
 
 #include "common.hpp"
@@ -318,37 +322,55 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
     }
   }
   __syncthreads();
-  uint16_t* out = isq ? p.q : p.k;
+  // The rotated tile goes through the (now free) ring as bf16 rows of kNT
+  // features, 16-byte pieces XOR-swizzled by row, and leaves it in 16-byte
+  // stores of whole rows (the accumulators hold one feature per lane).
+  static_assert(kMT * kNT * 2 <= kRingB, "output tile exceeds the ring");
+  constexpr int kOutRowB = kNT * 2;
+  auto out_slot = [&](int row, int col) {
+    return row * kOutRowB + ((((col * 2) >> 4) ^ (row & 7)) << 4) + ((col * 2) & 15);
+  };
   // rotary pairs of this wave's column list: slots c (a first-half block) and
   // cp (its partner, PB blocks on)
   auto rotate_pair = [&](auto ic) __attribute__((always_inline)) {
     constexpr int i = decltype(ic)::value;
     constexpr int c = CBW == 2 ? 0 : (D == 128 ? i : 2 * i);
     constexpr int cp = CBW == 2 ? 1 : c + PB;
+    const int col = 32 * cbl[c] + l32;  // tile feature of the first-half element; its partner is D/2 on
     const int d = (32 * cbl[c]) % D + l32;  // element of the first half of its head (d < D/2)
-    const int head = (n0 + 32 * cbl[c]) / D;
-    const double inv_freq = exp2(-(2.0 * d / D) * p.log2_theta);
+    const double turns_per_pos = exp2(-(2.0 * d / D) * p.log2_theta) * 0.15915494309189535;  // / (2 pi)
 #pragma unroll
     for (int rb = 0; rb < RB; ++rb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int row = 64 * wr + 32 * rb + acc_row(r, hl);
-        if (row < nrows && (isq || kflag[row])) {
-          const float f = rs[row];
-          const float x1 = acc[rb][c][r] * f, x2 = acc[rb][cp][r] * f;
-          // angle pos * theta^(-2d/D), reduced to [-pi, pi] in double
-          double a = (double)pos[row] * inv_freq;
-          a -= 6.283185307179586 * rint(a * 0.15915494309189535);
-          float sn, cs;
-          sincosf((float)a, &sn, &cs);
-          uint16_t* o = out + (((size_t)b * p.S + row0 + row) * H + head) * D;
-          o[d] = f32_to_bf16_bits(x1 * cs - x2 * sn);
-          o[d + D / 2] = f32_to_bf16_bits(x2 * cs + x1 * sn);
-        }
+        const float f = rs[row];
+        const float x1 = acc[rb][c][r] * f, x2 = acc[rb][cp][r] * f;
+        // angle pos * theta^(-2d/D) in turns, reduced to [-1/2, 1/2] in double;
+        // the hardware sine and cosine take turns
+        double t = (double)pos[row] * turns_per_pos;
+        t -= rint(t);
+        const float sn = __builtin_amdgcn_sinf((float)t), cs = __builtin_amdgcn_cosf((float)t);
+        *reinterpret_cast<uint16_t*>(lds + out_slot(row, col)) = f32_to_bf16_bits(x1 * cs - x2 * sn);
+        *reinterpret_cast<uint16_t*>(lds + out_slot(row, col + D / 2)) = f32_to_bf16_bits(x2 * cs + x1 * sn);
+        __builtin_amdgcn_sched_barrier(0);  // one row at a time: bounded live ranges
       }
   };
   rotate_pair(std::integral_constant<int, 0>{});
   if constexpr (CBW == 4) rotate_pair(std::integral_constant<int, 1>{});
+  __syncthreads();
+  // rows of the tile that exist and are kept (queries: every text row)
+  uint16_t* out = isq ? p.q : p.k;
+  constexpr int kPiecesPerRow = kOutRowB / 16;
+#pragma unroll
+  for (int j = 0; j < kMT * kPiecesPerRow / kTh; ++j) {
+    const int q = tid + kTh * j;
+    const int row = q / kPiecesPerRow, pc = q % kPiecesPerRow;
+    if (row < nrows && (isq || kflag[row])) {
+      const u32x4v v = *reinterpret_cast<const u32x4v*>(lds + row * kOutRowB + ((pc ^ (row & 7)) << 4));
+      *reinterpret_cast<u32x4v*>(out + ((size_t)b * p.S + row0 + row) * H * D + n0 + 8 * pc) = v;
+    }
+  }
 }
 
 // w_out[n, c] = bf16(w[n, c] * gamma[c]): the RMS normalisation gain folded
