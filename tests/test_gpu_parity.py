@@ -348,6 +348,33 @@ def test_fused_select_view_layouts(name, over):
     check_select(case, g, oracle.run_path(case, attention=False), name)
 
 
+@pytest.mark.parametrize("name,over,one_full", [
+    ("16 samples, the most the balanced split takes",
+     dict(B=16, N=4, Tv=96, T=12, Hq=8, Hkv=2, D=128, n_masked=(0, 3), keep_ratio=0.4), False),
+    ("251 key tiles per sample (8 views of 2000 + 16 text), D=64",
+     dict(B=2, N=8, Tv=2000, T=16, Hq=4, Hkv=1, D=64, n_masked=(0, 4), keep_ratio=0.3), False),
+    ("one sample keeps every view, five keep one",
+     dict(B=6, N=6, Tv=200, T=16, Hq=8, Hkv=2, D=128, n_masked=0, keep_ratio=0.5), True),
+])
+def test_fused_select_balanced_split_limits(name, over, one_full):
+    """The balanced sweep-1 split at its limits: the most samples it takes, a
+    sequence near its 256 key tiles, and a sample that keeps every view beside
+    samples that keep one (that sample takes the most splits). Against the
+    two-call path by the band rule, and the oracle's selection."""
+    case = synth.config_case(2, **over)
+    if one_full:
+        logit = np.full((case.B, case.N), -8.0, np.float32)
+        logit[0, :] = 8.0
+        logit[1:, 0] = 8.0
+        case = dataclasses.replace(case, view_logit=logit)
+    assert balanced_split(case), name
+    log(f"balanced split {name}: B={case.B} N={case.N} V_full={case.V_full} S={case.S}")
+    g = run_fused(case)
+    two = run_two_calls(case, case.keep_ratio, case.view_logit, None, case.w_lexical, case.threshold)
+    assert_same_select(g, two, name, case, exact=False)
+    check_select(case, g, oracle.run_path(case, attention=False), name)
+
+
 def test_fused_select_random_logits_lexical_fallback():
     """Logits near the threshold, lexical scores, and samples where no view
     passes (the best-view fallback): the in-call decision is the patch-select
