@@ -165,7 +165,7 @@ struct BalUnit {
 __device__ bool bal_unit(const ScoreDims& d, uint8_t* tmp, int w, int lane, BalUnit& u) {
   uint64_t* lm = reinterpret_cast<uint64_t*>(tmp);                      // [kBalMaxBatch][kBalWords]
   int* nl = reinterpret_cast<int*>(tmp + 8 * kBalMaxBatch * kBalWords);  // [kBalMaxBatch]
-  int* res = nl + kBalMaxBatch;                                          // b, g, rb, split, ntl, ns, a, valid
+  int* res = nl + kBalMaxBatch;                                          // b, g, rb, split, ntl, ns, -, valid
   int* lst = res + 8;                                                    // [64]
   if (w < d.B) {
     const uint32_t vm = (uint32_t)view_keep_mask<kFusedViews>(view_load(d.vs.logit, d.vs.lexical, d.vs.N, w, lane),
@@ -178,7 +178,8 @@ __device__ bool bal_unit(const ScoreDims& d, uint8_t* tmp, int w, int lane, BalU
       uint32_t live = k1 > d.V_full ? 1u : 0u;  // holds a text key
 #pragma unroll
       for (int v = 0; v < kFusedViews; ++v)  // bitwise, no branches: a kept view overlaps the tile
-        live |= (v < d.vs.N ? 1u : 0u) & (vm >> v) & (d.vs.off[v] < k1 ? 1u : 0u) & (d.vs.off[v + 1] > k0 ? 1u : 0u);
+        live |= (v < d.vs.N ? 1u : 0u) & ((vm >> v) & 1u) & (d.vs.off[v] < k1 ? 1u : 0u) &
+                (d.vs.off[v + 1] > k0 ? 1u : 0u);
       const uint64_t bits = __ballot((live & (t < d.n_kt ? 1u : 0u)) != 0u);
       cnt += __popcll(bits);
       if (lane == 0) lm[w * kBalWords + wd] = bits;
@@ -575,7 +576,10 @@ __device__ __forceinline__ int keys_upto(int L) {
 // running (max, sum) of exp2(logit) over the split's visible keys; the key
 // tiles stream through a ring of LDS buffers, dead tiles (dropped views only) are
 // not computed. Output: rowpart[b][g][split][row] = (max, sum), max in log2
-// units.
+// units. With d.bal (the view selection inside the call, 2..16 samples) the
+// same grid takes units of the balanced split instead (bal_unit): a split is
+// a list of live tiles, a sample has up to ns1 of them per column, and split 0
+// fills the slots its sample does not use with (-inf, 0).
 
 template <int DT, int D, bool VSEL>
 __global__ void __launch_bounds__(kSweepThreads)
