@@ -182,10 +182,19 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
  * paragraphs (the selected views' patches are what the token scoring sees);
  * the rest as for the two calls.
  *
- * The results are those of litevlm_patch_select (with these N, view offsets,
- * logits, lexical scores, w_lexical and threshold) followed by
- * litevlm_token_score_topk on its token mask, bit for bit: the same fp32
- * decision, evaluated by the same device code.
+ * The view decision (view_keep, the token mask, n_visual_kept) is that of
+ * litevlm_patch_select with these N, view offsets, logits, lexical scores,
+ * w_lexical and threshold, bit for bit: the same fp32 decision, evaluated by
+ * the same device code. The rest is litevlm_token_score_topk on that token
+ * mask:
+ *   - bit for bit for B = 1;
+ *   - for 2 <= B <= 16 the first score sweep splits the live key tiles (those
+ *     of kept views, and the text) in proportion over the samples. That split
+ *     follows from the view masks, which this call has and the two-call path
+ *     does not. Its partial sums round differently, so a score may differ
+ *     from the two-call path in its last bits (well within 1e-5 relative), and
+ *     the kept set only where scores tie within such a difference.
+ * Both paths are deterministic.
  *
  *   N                  views, 1..LITEVLM_MAX_FUSED_VIEWS (N up to LITEVLM_MAX_VIEWS:
  *                      LITEVLM_ERR_UNSUPPORTED; use the two calls)
