@@ -188,8 +188,11 @@ litevlm_status_t litevlm_token_score_topk(int32_t dtype, int32_t B, int32_t S, i
  * the same device code. The rest is litevlm_token_score_topk on that token
  * mask:
  *   - bit for bit for B = 1;
- *   - for 2 <= B <= 16 the first score sweep splits the live key tiles (those
- *     of kept views, and the text) in proportion over the samples. That split
+ *   - for 2 <= B <= 16 (where the shape gives the first sweep at least two
+ *     key splits per (sample, KV group, 512-row block) and at most 256 key
+ *     tiles of 64 per sample; bit for bit otherwise) the first score sweep
+ *     splits the live key tiles (those of kept views, and the text) in
+ *     proportion over the samples. That split
  *     follows from the view masks, which this call has and the two-call path
  *     does not. Its partial sums round differently, so a score may differ
  *     from the two-call path in its last bits (well within 1e-5 relative), and
