@@ -355,13 +355,17 @@ def test_fused_select_view_layouts(name, over):
      dict(B=2, N=8, Tv=2000, T=16, Hq=4, Hkv=1, D=64, n_masked=(0, 4), keep_ratio=0.3), False),
     ("one sample keeps every view, five keep one",
      dict(B=6, N=6, Tv=200, T=16, Hq=8, Hkv=2, D=128, n_masked=0, keep_ratio=0.5), True),
+    ("two 512-row blocks per (sample, KV group): 160 text tokens x 4 heads",
+     dict(B=2, N=4, Tv=128, T=160, Hq=8, Hkv=2, D=128, n_masked=(0, 2), keep_ratio=0.5), False),
+    ("fp32, 3 samples", dict(cfg=1, B=3, N=3, Tv=64, T=16, n_masked=(0, 1), keep_ratio=0.5), False),
 ])
 def test_fused_select_balanced_split_limits(name, over, one_full):
     """The balanced sweep-1 split at its limits: the most samples it takes, a
     sequence near its 256 key tiles, and a sample that keeps every view beside
     samples that keep one (that sample takes the most splits). Against the
     two-call path by the band rule, and the oracle's selection."""
-    case = synth.config_case(2, **over)
+    over = dict(over)
+    case = synth.config_case(over.pop("cfg", 2), **over)
     if one_full:
         logit = np.full((case.B, case.N), -8.0, np.float32)
         logit[0, :] = 8.0
