@@ -379,6 +379,19 @@ def test_fused_select_balanced_split_limits(name, over, one_full):
     check_select(case, g, oracle.run_path(case, attention=False), name)
 
 
+def test_fused_select_beyond_balanced_split():
+    """17 samples, one past the balanced split's limit: the first sweep splits
+    tile ranges evenly again, and the in-call selection equals the two calls
+    bit for bit (and the oracle's selection)."""
+    case = synth.config_case(2, B=17, N=4, Tv=96, T=12, Hq=8, Hkv=2, D=128, n_masked=(0, 3), keep_ratio=0.4)
+    assert not balanced_split(case)
+    log(f"beyond the balanced split: B={case.B} N={case.N} V_full={case.V_full} S={case.S}")
+    g = run_fused(case)
+    two = run_two_calls(case, case.keep_ratio, case.view_logit, None, case.w_lexical, case.threshold)
+    assert_same_select(g, two, "B=17", case, exact=True)
+    check_select(case, g, oracle.run_path(case, attention=False), "B=17")
+
+
 def test_fused_select_random_logits_lexical_fallback():
     """Logits near the threshold, lexical scores, and samples where no view
     passes (the best-view fallback): the in-call decision is the patch-select
