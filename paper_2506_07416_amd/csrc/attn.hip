@@ -771,12 +771,17 @@ attn_fp8_kernel(AttnParams p) {
   const int qi = m0 + w * 32 + lq;
   const int wave_q0 = m0 + w * 32;
 
-  // piece swizzles (involutions): K reads hit 16 rows x 1 piece per 16 lanes,
-  // V transposed reads 8 rows x 1 piece per 16 lanes
+  // piece swizzles (involutions): K reads hit 16 rows x 1 piece per 16 lanes;
+  // V transposed reads (8 bytes a lane, 32 lanes a cycle) hit 8 rows x the 2
+  // pieces 2*db, 2*db+1 per 32 lanes. With 128-byte rows, rows r and r^1 fill
+  // the two halves of the 256-byte bank window, and piece p of row r sits at
+  // p ^ (r & 6): pieces (2*db + e) ^ 2i = 2*(db ^ i) + e are distinct over the
+  // 4 row pairs i and both halves e, so the 32 lanes hit 32 distinct 8-byte
+  // slots.
   auto kswz = [](int r) {
     return NP >= 8 ? (((r >> 1) & 3) | (((r >> 5) & 1) << 2)) : (((r >> 2) & 1) | (((r >> 5) & 1) << 1));
   };
-  auto vswz = [](int r) { return (r >> 1) & (NP - 1) & 3; };
+  auto vswz = [](int r) { return NP >= 8 ? (r & 6) : ((r >> 1) & (NP - 1) & 3); };
 
   // Copy j of a wave moves 16-byte pieces of tile row ld_row[j]; its source
   // is (tile base, wave-uniform) + ld_koff[j] / ld_voff[j] (per lane, fixed).
@@ -808,7 +813,7 @@ attn_fp8_kernel(AttnParams p) {
 #pragma unroll
   for (int db = 0; db < DB; ++db)
     voff[db] = vrow0 * RB + (((2 * db + (g16 & 1)) ^ vswz(vrow0)) * 16) + (s16 & 1) * 8;
-  // rows vrow0 + 8*j share vswz: (r>>1)&3 depends on bits 1,2 only
+  // rows vrow0 + 8*j share vswz: it depends on bits 1, 2 of the row only
 
   auto copy_tile = [&](int tile, auto bufc) __attribute__((always_inline)) {
     constexpr int BUF = decltype(bufc)::value;
