@@ -98,6 +98,40 @@ __device__ __forceinline__ bool decode_work(const AttnParams& p, int& b, int& h,
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
+// Output of a wave's 32 query rows: o[db][r] holds element db*32 +
+// acc_row32(r, hl) of row lane % 32 (the O^T accumulators). The block goes
+// through the wave's 32 rows of free LDS at ob (2*D bytes a row) as bf16,
+// 16-byte pieces XOR-swizzled by row, and leaves in 16-byte stores of whole
+// rows, 2*D/16 lanes a row (rather than 8-byte pieces scattered over 32 rows):
+// row i < nrows goes to out + i*stride. LDS operations of one wave complete in
+// order, so the reads see the writes without a wait of their own; the caller
+// guarantees that no other wave uses these LDS rows meanwhile and that no copy
+// into them is in flight.
+template <int D>
+__device__ __forceinline__ void store_rows_bf16(const f32x16 (&o)[D / 32], float inv, uint8_t* ob, int lane, int nrows,
+                                                uint16_t* out, size_t stride) {
+  constexpr int ORB = 2 * D, OP = ORB / 16;  // bytes and 16-byte pieces per output row
+  const int lq = lane & 31, hl = lane >> 5;
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int q4 = 0; q4 < 4; ++q4) {
+      // accumulator rows 4*q4 .. 4*q4+3: elements db*32 + 8*q4 + 4*hl + 0..3
+      const u32x2 v = {(uint32_t)f32_to_bf16_bits(o[db][4 * q4] * inv) |
+                           ((uint32_t)f32_to_bf16_bits(o[db][4 * q4 + 1] * inv) << 16),
+                       (uint32_t)f32_to_bf16_bits(o[db][4 * q4 + 2] * inv) |
+                           ((uint32_t)f32_to_bf16_bits(o[db][4 * q4 + 3] * inv) << 16)};
+      const int piece = 4 * db + q4;
+      *reinterpret_cast<u32x2*>(ob + lq * ORB + ((piece ^ (lq & (OP - 1))) * 16) + 8 * hl) = v;
+    }
+#pragma unroll
+  for (int i = 0; i < 32 * OP / 64; ++i) {
+    const int pc = lane + 64 * i, row = pc / OP, col = pc % OP;
+    const u32x4 v = *reinterpret_cast<const u32x4*>(ob + row * ORB + ((col ^ (row & (OP - 1))) * 16));
+    if (row < nrows) *reinterpret_cast<u32x4*>(out + (size_t)row * stride + col * 8) = v;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // bf16 path: 4 waves x 32 query rows of one head per workgroup, 64-key tiles
 // double-buffered in LDS. Tiles are copied global -> LDS directly
@@ -352,7 +386,11 @@ attn_bf16_kernel(AttnParams p) {
 
   const float l = sum_xor32(l_run);
   const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
-  if (qi < len) {
+  if constexpr (OUT == LITEVLM_BF16) {
+    static_assert(sizeof(kvl) >= 4 * 32 * 2 * D, "the output rows of the 4 waves fit the tile buffers");
+    store_rows_bf16<D>(o, inv, kvl + w * 32 * (2 * D), lane, len - wave_q0,
+                       static_cast<uint16_t*>(p.o) + ((size_t)(seq0 + wave_q0) * p.Hq + h) * D, (size_t)p.Hq * D);
+  } else if (qi < len) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
@@ -710,7 +748,11 @@ attn_bf16_pipe_kernel(AttnParams p) {
 
   const float l = sum_xor32(l_run);
   const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
-  if (qi < len) {
+  if constexpr (OUT == LITEVLM_BF16) {
+    static_assert(sizeof(kvl) >= 4 * 32 * 2 * D, "the output rows of the 4 waves fit the tile buffers");
+    store_rows_bf16<D>(o, inv, kvl + w * 32 * (2 * D), lane, len - wave_q0,
+                       static_cast<uint16_t*>(p.o) + ((size_t)(seq0 + wave_q0) * p.Hq + h) * D, (size_t)p.Hq * D);
+  } else if (qi < len) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
