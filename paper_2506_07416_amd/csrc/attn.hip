@@ -151,6 +151,13 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | ((N >> 4) << 14) | (0x7 << 4) | (0xF << 8));
 }
 
+// Workgroup barrier with only the LDS wait spelled out (the copies in flight
+// are waited for explicitly by the caller; the fence of __syncthreads would
+// wait for all of them). The memory clobber keeps LDS accesses on their side.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
 template <int D, bool CAUSAL, int OUT>
 __global__ void __launch_bounds__(256, 2)
 attn_bf16_kernel(AttnParams p) {
@@ -237,13 +244,27 @@ attn_bf16_kernel(AttnParams p) {
     }
   };
 
-  bf16x8 qreg[KS];
+  // ---- queries: the wave's 32 rows are copied whole (NP lanes a row, so each
+  // copy reads 1 KB of contiguous rows) into its quarter of the second K/V
+  // buffers, free until step 0 refills them, with 16-byte pieces XOR-swizzled
+  // by row; each lane then reads its operand registers (row lq, pieces
+  // 2*ks + hl) from there. Read straight from memory, every load of the
+  // operand layout would touch 32 rows at 32 bytes each.
+  uint8_t* qst = kvl + (w < 2 ? TB : 3 * TB) + (w & 1) * (32 * RB);  // 32 rows of this wave
   {
-    const uint8_t* qr = static_cast<const uint8_t*>(p.q) + ((size_t)(seq0 + min(qi, len - 1)) * p.Hq + h) * RB;
+    constexpr int QRI = 1024 / RB;  // rows per 1 KB copy
+    const int r_in = lane / NP, ph = lane % NP;
+    const uint32_t lds_q = __builtin_amdgcn_readfirstlane((uint32_t)(qst - kvl));
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-      qreg[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qr + (ks * 16 + 8 * hl) * 2));
+    for (int j = 0; j < 32 / QRI; ++j) {
+      const int r = QRI * j + r_in;
+      const uint8_t* src = static_cast<const uint8_t*>(p.q) +
+                           ((size_t)(seq0 + min(wave_q0 + r, len - 1)) * p.Hq + h) * RB + ((ph ^ (r & (NP - 1))) * 16);
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(kvl + lds_q + j * 1024), 16, 0, 0);
+    }
   }
+  __builtin_amdgcn_sched_barrier(0);
   f32x16 o[DB];
 #pragma unroll
   for (int db = 0; db < DB; ++db)
@@ -255,8 +276,13 @@ attn_bf16_kernel(AttnParams p) {
   const int nt = (kend + BN - 1) / BN;
 
   copy_tile(0, std::integral_constant<int, 0>{});
-  wait_vmcnt<0>();
-  __syncthreads();
+  wait_vmcnt<0>();  // this wave's copies have landed: its own query rows may be read
+  bf16x8 qreg[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks)
+    qreg[ks] = __builtin_bit_cast(bf16x8, *reinterpret_cast<const u32x4*>(qst + lq * RB + (((2 * ks + hl) ^ (lq & (NP - 1))) * 16)));
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();  // tile 0 has landed for every wave, and every wave has its queries (step 0 refills the second buffers)
 
   // step t (K, V of tile t in buffers BUF = t & 1); instantiated per buffer so
   // that every LDS offset is an immediate
@@ -388,7 +414,9 @@ attn_bf16_kernel(AttnParams p) {
   const float inv = (l > 0.f) ? p.out_scale / l : 0.f;
   if constexpr (OUT == LITEVLM_BF16) {
     static_assert(sizeof(kvl) >= 4 * 32 * 2 * D, "the output rows of the 4 waves fit the tile buffers");
-    store_rows_bf16<D>(o, inv, kvl + w * 32 * (2 * D), lane, len - wave_q0,
+    int lane_e = lane;  // opaque: the epilogue's offsets are not shared with (kept live from) the prologue's
+    asm volatile("" : "+v"(lane_e));
+    store_rows_bf16<D>(o, inv, kvl + w * 32 * (2 * D), lane_e, len - wave_q0,
                        static_cast<uint16_t*>(p.o) + ((size_t)(seq0 + wave_q0) * p.Hq + h) * D, (size_t)p.Hq * D);
   } else if (qi < len) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
@@ -427,13 +455,6 @@ attn_bf16_kernel(AttnParams p) {
 // per SIMD.
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-
-// Workgroup barrier with only the LDS wait spelled out (the copies in flight
-// are waited for explicitly by the caller; the fence of __syncthreads would
-// wait for all of them). The memory clobber keeps LDS accesses on their side.
-__device__ __forceinline__ void lds_barrier() {
-  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
-}
 
 // Transposed LDS read (ds_read_b64_tr_b16) as inline assembly: the builtin
 // makes the compiler wait for every direct copy in flight before it, which
