@@ -1017,7 +1017,13 @@ attn_fp8_kernel(AttnParams p) {
 
   const float l = lsum[0];
   const float inv = (l > 0.f) ? p.out_scale / l : 0.f;   // l already carries 2^PSHIFT
-  if (qi < len) {
+  if constexpr (OUT == LITEVLM_BF16 && CAUSAL) {  // (the non-causal instance would spill)
+    static_assert(sizeof(kvl) >= 4 * 32 * 2 * D, "the output rows of the 4 waves fit the tile buffers");
+    int lane_e = lane;  // opaque: the epilogue's offsets are not shared with (kept live from) the prologue's
+    asm volatile("" : "+v"(lane_e));
+    store_rows_bf16<D>(o, inv, kvl + w * 32 * (2 * D), lane_e, len - wave_q0,
+                       static_cast<uint16_t*>(p.o) + ((size_t)(seq0 + wave_q0) * p.Hq + h) * D, (size_t)p.Hq * D);
+  } else if (qi < len) {
     const size_t obase = ((size_t)(seq0 + qi) * p.Hq + h) * D;
 #pragma unroll
     for (int db = 0; db < DB; ++db)
