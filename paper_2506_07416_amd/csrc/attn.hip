@@ -138,7 +138,7 @@ __device__ __forceinline__ void store_rows_bf16(const f32x16 (&o)[D / 32], float
 // (global_load_lds_dwordx4, no VGPR staging) into XOR-swizzled rows so that
 // the MFMA operand reads are bank-conflict free; V stays row-major and is read
 // transposed with ds_read_b64_tr_b16. Every per-lane offset is computed once,
-// outside the key loop. ~210 VGPRs, so two waves share each SIMD and one
+// outside the key loop. Under 256 VGPRs, so two waves share each SIMD and one
 // wave's softmax overlaps the other's matrix work.
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
