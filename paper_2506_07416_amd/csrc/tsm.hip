@@ -68,7 +68,8 @@ struct TsmParams {
   uint16_t* q;          // bf16 [B, S, Hq, D]
   uint16_t* k;          // bf16 [B, S, Hkv, D]
   int B, S, V_full, Dm, Hq, Hkv;
-  int mk, nk, mq, nq, n_k_items, n_items, per_xcd;
+  int mk, nk, mq, nq, gk, gq, per_xcd;  // gk, gq: key and query row tiles (B*mk, B*mq)
+  int compact;                          // deal the working key row tiles by rank (kMT = 256 only)
   float eps;
   double log2_theta;
 };
@@ -108,24 +109,97 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
   constexpr int PB = D / 64;     // column-block distance of rotary partners
   constexpr int RB = 2;          // 32-row blocks per wave
   constexpr int CBW = Tl::kCBW;  // 32-column blocks per wave
-  const int L = blockIdx.x;
-  const int item = (L & 7) * p.per_xcd + (L >> 3);  // an XCD takes a contiguous item range
-  if (item >= p.n_items) return;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tl::kLdsB];
+  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   bool isq;
   int b, mt, nt;
-  if (item < p.n_k_items) {
-    isq = false;
-    b = item / (p.mk * p.nk);
-    const int r = item % (p.mk * p.nk);
-    mt = r / p.nk;
-    nt = r % p.nk;
+  if (MT == 256 && p.compact) {
+    // Only the key row tiles that hold a kept row produce anything. Every
+    // workgroup finds them from the keep bytes (one wave per tile in turn,
+    // four bytes a lane) and deals them, with their feature tiles, to the
+    // XCDs round robin by rank: each XCD gets the same number of working
+    // items whatever the dropped views, and a row tile's feature tiles stay on
+    // one XCD (they share its rows of x in that L2). The query items follow,
+    // continuing the rotation. The flags go into the ring, unused until the
+    // stage copies start.
+    uint8_t* gf = lds;
+    for (int g0 = 0; g0 < p.gk; g0 += 8 * NW) {
+      uint32_t any8 = 0;
+      uint8_t kb[8][4];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int g = g0 + u * NW + w;
+        const int gb = g / p.mk, r0 = (g % p.mk) * kMT;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int r = r0 + lane + 64 * e;  // kMT = 256 rows: 64 lanes x 4
+          kb[u][e] = (g < p.gk && r < p.S) ? p.keep[(size_t)gb * p.S + r] : 0;
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const bool kept = (kb[u][0] | kb[u][1] | kb[u][2] | kb[u][3]) != 0;
+        any8 |= (__ballot(kept) != 0ull ? 1u : 0u) << u;
+      }
+      if (lane == 0) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+          const int g = g0 + u * NW + w;
+          if (g < p.gk) gf[g] = (uint8_t)((any8 >> u) & 1u);
+        }
+      }
+    }
+    __syncthreads();
+    // the working tile of rank x + 8*(j / nk), and the number of working tiles
+    // (every wave computes the same values)
+    const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+    const int rk = x + 8 * (j / p.nk);
+    int nwork = 0, grp = 0;
+    for (int c0 = 0; c0 < p.gk; c0 += 64) {
+      const bool f = c0 + lane < p.gk && gf[c0 + lane] != 0;
+      const uint64_t m = __ballot(f);
+      const int cnt = __popcll(m);
+      if (rk >= nwork && rk < nwork + cnt) {
+        const int before = __popcll(m & ((1ull << lane) - 1ull));
+        const uint64_t sel = __ballot(f && before == rk - nwork);
+        grp = c0 + __ffsll((unsigned long long)sel) - 1;
+      }
+      nwork += cnt;
+    }
+    const int ck = nwork > x ? (nwork - x + 7) / 8 : 0;  // working key tiles of this XCD
+    if (j < ck * p.nk) {
+      isq = false;
+      b = grp / p.mk;
+      mt = grp % p.mk;
+      nt = j % p.nk;
+    } else {
+      const int qi = (x - nwork % 8 + 8) % 8 + 8 * (j - ck * p.nk);
+      if (qi >= p.gq * p.nq) return;
+      isq = true;
+      b = qi / (p.mq * p.nq);
+      const int r = qi % (p.mq * p.nq);
+      mt = r / p.nq;
+      nt = r % p.nq;
+    }
   } else {
-    const int j = item - p.n_k_items;
-    isq = true;
-    b = j / (p.mq * p.nq);
-    const int r = j % (p.mq * p.nq);
-    mt = r / p.nq;
-    nt = r % p.nq;
+    // an XCD takes a contiguous item range
+    const int item = (blockIdx.x & 7) * p.per_xcd + (blockIdx.x >> 3);
+    const int n_k_items = p.gk * p.nk;
+    if (item >= n_k_items + p.gq * p.nq) return;
+    if (item < n_k_items) {
+      isq = false;
+      b = item / (p.mk * p.nk);
+      const int r = item % (p.mk * p.nk);
+      mt = r / p.nk;
+      nt = r % p.nk;
+    } else {
+      const int jq = item - n_k_items;
+      isq = true;
+      b = jq / (p.mq * p.nq);
+      const int r = jq % (p.mq * p.nq);
+      mt = r / p.nq;
+      nt = r % p.nq;
+    }
   }
   const int row0 = (isq ? p.V_full : 0) + mt * kMT;  // first row of the tile within the sample
   const int nrows = min(kMT, p.S - row0);
@@ -134,13 +208,11 @@ __global__ __launch_bounds__(64 * NW, (TsmTile<MT, NT, NW>::kWgPerCu)) void tsm_
   const int H = isq ? p.Hq : p.Hkv;
   const int Dm = p.Dm;
 
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[Tl::kLdsB];
   float* rs = reinterpret_cast<float*>(lds + kRingB);
   int* pos = reinterpret_cast<int*>(lds + kRingB + kMT * 4);
   int* red = reinterpret_cast<int*>(lds + kRingB + kMT * 8);
   uint8_t* kflag = lds + kRingB + kMT * 8 + 128;
 
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int wr = w % NWR, wc = w / NWR, hl = lane >> 5, l32 = lane & 31;
 
   // ---- positions of the tile's rows in the patch-selected sequence
@@ -407,9 +479,10 @@ hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream) {
     p.nk = a.Hkv * a.D / NT;
     p.mq = (T + MT - 1) / MT;
     p.nq = a.Hq * a.D / NT;
-    p.n_k_items = a.B * p.mk * p.nk;
-    p.n_items = p.n_k_items + a.B * p.mq * p.nq;
-    p.per_xcd = (p.n_items + 7) / 8;
+    p.gk = a.B * p.mk;
+    p.gq = a.B * p.mq;
+    p.compact = 0;
+    p.per_xcd = (p.gk * p.nk + p.gq * p.nq + 7) / 8;
     return dim3(8 * p.per_xcd);
   };
   // 256 x 256 tiles (8 waves, one workgroup per CU) halve the L2 traffic per
@@ -417,7 +490,13 @@ hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream) {
   const bool big = (a.Hkv * a.D) % 256 == 0 && (a.Hq * a.D) % 256 == 0 &&
                    (int64_t)a.B * ((a.S + 255) / 256) * (a.Hkv * a.D / 256) >= 256;
   if (big) {
-    const dim3 grid = setup(256, 256);
+    dim3 grid = setup(256, 256);
+    if (a.token_keep) {
+      // at most (gk+7)/8 working key row tiles per XCD, and (gq*nq+7)/8 query items
+      p.compact = 1;
+      p.per_xcd = (p.gk + 7) / 8 * p.nk + (p.gq * p.nq + 7) / 8;
+      grid = dim3(8 * p.per_xcd);
+    }
     if (a.D == 128) hipLaunchKernelGGL((tsm_proj_kernel<128, 256, 256, 8>), grid, dim3(512), 0, stream, p);
     else hipLaunchKernelGGL((tsm_proj_kernel<64, 256, 256, 8>), grid, dim3(512), 0, stream, p);
   } else {
