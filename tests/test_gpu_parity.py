@@ -201,6 +201,11 @@ SELECT_CASES = [
     ("gather-w5", dict(cfg=2, Tv=32, T=8, Hq=48, Hkv=12, D=128)),
     ("gather-w9", dict(cfg=2, Tv=32, T=8, Hq=48, Hkv=48, D=128)),
     ("gather-w32-f32", dict(cfg=1, Tv=40, T=6, Hq=128, Hkv=64, D=128)),
+    # the largest inputs the calls take: LITEVLM_MAX_VISUAL visual tokens (8
+    # views of 2048), and LITEVLM_MAX_BATCH samples
+    ("max-visual", dict(cfg=2, N=8, Tv=2048, T=16, Hq=8, Hkv=2, D=64, keep_ratio=0.25)),
+    ("max-batch", dict(cfg=4, B=256, N=2, Tv=16, T=4, Hq=2, Hkv=1, D=64, n_masked=(0, 1),
+                       salient=(0.1, 0.3), keep_ratio=0.5)),
 ]
 
 
@@ -335,11 +340,16 @@ def test_fused_select_equals_two_calls(cfg, r):
      dict(B=3, N=3, Tv=43, T=7, Hq=4, Hkv=2, D=64, n_masked=1, keep_ratio=0.4)),
     ("one view", dict(B=2, N=1, Tv=100, T=9, Hq=8, Hkv=2, D=128, n_masked=0, keep_ratio=0.5)),
     ("8 views of 24, up to 4 masked", dict(B=4, N=8, Tv=24, T=5, Hq=8, Hkv=8, D=128, n_masked=4, keep_ratio=0.7)),
+    ("the most visual tokens: 8 views of 2048 (V_full = 16384), D=64",
+     dict(B=1, N=8, Tv=2048, T=16, Hq=8, Hkv=2, D=64, n_masked=2, keep_ratio=0.25)),
+    ("the most samples: 256 x (2 views of 16 + 4 text), D=64",
+     dict(B=256, N=2, Tv=16, T=4, Hq=2, Hkv=1, D=64, n_masked=(0, 1), keep_ratio=0.5)),
 ])
 def test_fused_select_view_layouts(name, over):
     """View boundaries off the 4-key vectors and the 64-key tiles, a single
-    view, the most views the in-call selection takes: bit for bit the two-call
-    path, and the oracle's selection."""
+    view, the most views the in-call selection takes, the most visual tokens
+    and samples the calls take: bit for bit the two-call path, and the
+    oracle's selection."""
     case = synth.config_case(2, **over)
     log(f"fused select {name}: B={case.B} N={case.N} V_full={case.V_full} S={case.S}")
     g = run_fused(case)
