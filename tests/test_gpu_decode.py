@@ -53,6 +53,8 @@ CASES = [
     ("f32 long splits", [1100, 3, 1024, 900, 1, 64, 1000, 1100], 32, 8, 128, "f32", True, 0, None),
     ("fp8 GQA4 D128", [0, 65, 700, 1500], 32, 8, 128, "fp8", True, 0, None),
     ("fp8 GQA2 D64 long splits", [2100, 10, 2000, 1800, 600, 2100, 5, 2050], 16, 8, 64, "fp8", True, 0, None),
+    # LITEVLM_MAX_BATCH samples, cache lengths 0..300 (empty ones included)
+    ("bf16 256 samples", [(37 * i) % 301 for i in range(256)], 8, 2, 64, "bf16", True, 0, None),
 ]
 
 
