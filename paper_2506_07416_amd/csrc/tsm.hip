@@ -491,7 +491,9 @@ hipError_t launch_tsm_qk(const TsmArgs& a, hipStream_t stream) {
                    (int64_t)a.B * ((a.S + 255) / 256) * (a.Hkv * a.D / 256) >= 256;
   if (big) {
     dim3 grid = setup(256, 256);
-    if (a.token_keep) {
+    // the dealing workgroups keep one flag byte per key row tile in the stage
+    // ring: longer batches take the contiguous ranges
+    if (a.token_keep && p.gk <= TsmTile<256, 256, 8>::kRingB) {
       // at most (gk+7)/8 working key row tiles per XCD, and (gq*nq+7)/8 query items
       p.compact = 1;
       p.per_xcd = (p.gk + 7) / 8 * p.nk + (p.gq * p.nq + 7) / 8;

@@ -69,6 +69,9 @@ def check(got, ref, what):
     ("ragged rows, D=64, GQA 8/2", dict(B=1, N=2, Tv=100, T=37, Hq=8, Hkv=2, D=64, n_masked=0), 192),
     ("MHA 16/16 D=128, 2 of 6 views dropped", dict(B=1, N=6, Tv=40, T=64, Hq=16, Hkv=16, D=128,
                                                    n_masked=2), 512),
+    # LITEVLM_MAX_BATCH samples: 256 key row tiles of 256, the tiles dealt by rank
+    ("256 samples of 2 views x 48 + 16 text, GQA 4/2", dict(B=256, N=2, Tv=48, T=16, Hq=4, Hkv=2, D=128,
+                                                           n_masked=(0, 1)), 256),
 ])
 def test_tsm_matches_oracle(name, over, Dm):
     case = synth.config_case(2, **over)
